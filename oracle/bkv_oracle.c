@@ -1,0 +1,377 @@
+/*
+ * CPU oracle for the BeaconKV eviction step -- TEST INFRASTRUCTURE ONLY.
+ *
+ * This file is the plain, slow, obviously-correct statement of what the GPU
+ * library computes.  It exists so that tests, the smoke check and the
+ * benchmark's CPU baseline can compare against it.  Product code never links,
+ * loads or calls it, and it shares no source with the GPU path.
+ *
+ * Paper: "BeaconKV: Key-Value Cache Compression Guided by Beacon Queries for
+ * Efficient Large Reasoning Model Inference" (arXiv 2609.04971).
+ *
+ * Everything is computed per (batch, kv-head) pair on the exact values of
+ * the inputs (bf16 and fp32 widen exactly to double); arithmetic is double
+ * precision unless a step is defined in fp32 below.  Build with
+ * -ffp-contract=off: the RoPE step relies on separately rounded fp32
+ * multiplies and adds.
+ *
+ * Pins (what checks this file against something other than itself) live in
+ * tests/test_oracle_*.py: hand-worked examples, closed forms, library
+ * special cases (scipy log_softmax, numpy mean), brute force and invariants.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_F32 0
+#define ORC_BF16 1
+
+/* ---- element access --------------------------------------------------- */
+
+/* bf16 is the upper half of an IEEE binary32, so widening is a shift. */
+static float bf16_bits_to_float(uint16_t h) {
+    uint32_t u = ((uint32_t)h) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* Round a binary32 to the nearest bf16, ties to even (NaN stays NaN). */
+static float round_to_bf16(float f) {
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) {
+        u |= 0x00400000u; /* quiet NaN */
+        u &= 0xffff0000u;
+    } else {
+        uint32_t lsb = (u >> 16) & 1u;
+        u += 0x7fffu + lsb;
+        u &= 0xffff0000u;
+    }
+    float r;
+    memcpy(&r, &u, sizeof r);
+    return r;
+}
+
+static double elem(const void* base, size_t i, int dtype) {
+    if (dtype == ORC_BF16) return (double)bf16_bits_to_float(((const uint16_t*)base)[i]);
+    return (double)((const float*)base)[i];
+}
+
+/* ---- (a1) beacon maintenance --------------------------------------------
+ *
+ * Beacons are representatives of clusters of pre-RoPE queries compared by
+ * cosine similarity (Section 3.2 "Beacon queries"; the cosine geometry of
+ * Section 4.2 and the nearest-representative similarity S_j of Appendix D.1,
+ * Algorithm 1).  The online rule built here: every new query joins the beacon
+ * it is most cosine-similar to and that beacon becomes the running mean of
+ * its members (sequential k-means; a streaming form of the "K-Means
+ * Centroids" selector the paper compares in Figure 7).  Empty slots are
+ * seeded first, lowest slot first, so counts always sum to queries seen.
+ *
+ * One kv-head: q_block holds the G query heads of the group, [G][T][D];
+ * queries are taken in order t-major, then g ascending, and each one sees
+ * the beacons left by the previous one.  cos(x, b) = x.b / (|x||b|), and 0
+ * when either norm is 0.  argmax ties go to the lowest slot.  A near tie
+ * (best two cosines within 1e-6) is flagged in near_tie.
+ * The mean is formed in double and stored back to fp32 after every query.
+ * ------------------------------------------------------------------------ */
+int orc_beacon_update(int dtype, int D, int C, int G, int T, const void* q_block,
+                      float* beacons, int32_t* counts, int32_t* assign, int32_t* near_tie) {
+    if (D <= 0 || C <= 0 || G <= 0 || T < 0) return -1;
+    double* x = (double*)malloc(sizeof(double) * (size_t)D);
+    if (!x) return -2;
+    int q = 0;
+    for (int t = 0; t < T; ++t) {
+        for (int g = 0; g < G; ++g, ++q) {
+            for (int d = 0; d < D; ++d) x[d] = elem(q_block, ((size_t)g * T + t) * D + d, dtype);
+            int chosen = -1, tie = 0;
+            for (int c = 0; c < C; ++c) {
+                if (counts[c] == 0) { chosen = c; break; }
+            }
+            if (chosen >= 0) {
+                for (int d = 0; d < D; ++d) beacons[(size_t)chosen * D + d] = (float)x[d];
+                counts[chosen] = 1;
+            } else {
+                double xn = 0.0;
+                for (int d = 0; d < D; ++d) xn += x[d] * x[d];
+                xn = sqrt(xn);
+                double best = -INFINITY, second = -INFINITY;
+                for (int c = 0; c < C; ++c) {
+                    const float* b = beacons + (size_t)c * D;
+                    double dot = 0.0, bn = 0.0;
+                    for (int d = 0; d < D; ++d) {
+                        dot += x[d] * (double)b[d];
+                        bn += (double)b[d] * (double)b[d];
+                    }
+                    bn = sqrt(bn);
+                    double cs = (xn == 0.0 || bn == 0.0) ? 0.0 : dot / (xn * bn);
+                    if (cs > best) {
+                        second = best;
+                        best = cs;
+                        chosen = c;
+                    } else if (cs > second) {
+                        second = cs;
+                    }
+                }
+                tie = (C > 1) && (best - second <= 1e-6);
+                int32_t n = ++counts[chosen];
+                float* b = beacons + (size_t)chosen * D;
+                for (int d = 0; d < D; ++d) {
+                    double bd = (double)b[d];
+                    b[d] = (float)(bd + (x[d] - bd) / (double)n);
+                }
+            }
+            if (assign) assign[q] = chosen;
+            if (near_tie) near_tie[q] = tie;
+        }
+    }
+    free(x);
+    return 0;
+}
+
+/* ---- (a2) observation rows ------------------------------------------------
+ *
+ * Beacon queries are rotated to the current step t, recent queries keep their
+ * own positions (Section 4.3 "Query Construction and Alignment"; Algorithm 2,
+ * the construction of Q_obs).  Recent queries arrive already rotated.  RoPE is
+ * the rotate-half form: pair (d, d + D/2) is turned by the angle whose
+ * cosine and sine the caller tabulates for step t.
+ *
+ * Reading of the precision: each product is rounded to fp32, then the sum or
+ * difference is rounded to fp32 (no fused multiply-add), and for bf16 caches
+ * the row is then rounded to bf16 (nearest, ties to even).  A NULL table is
+ * the identity.  Only occupied slots (count > 0) become rows, in slot order;
+ * the G*W recent rows follow, g-major, w-minor.
+ * ------------------------------------------------------------------------ */
+void orc_rope_row(int D, const float* beta, const float* cos_t, const float* sin_t, int to_bf16,
+                  float* out) {
+    int h = D / 2;
+    for (int d = 0; d < h; ++d) {
+        float lo, hi;
+        if (cos_t && sin_t) {
+            float a = beta[d] * cos_t[d];
+            float b = beta[d + h] * sin_t[d];
+            float c = beta[d + h] * cos_t[d];
+            float e = beta[d] * sin_t[d];
+            lo = a - b;
+            hi = c + e;
+        } else {
+            lo = beta[d];
+            hi = beta[d + h];
+        }
+        out[d] = to_bf16 ? round_to_bf16(lo) : lo;
+        out[d + h] = to_bf16 ? round_to_bf16(hi) : hi;
+    }
+}
+
+/* Y is [(C + G*W)][D]; row_slot[r] names the slot a row came from: the
+ * beacon index c, or C + g*W + w for a recent query.  Returns R. */
+int orc_assemble_rows(int dtype, int D, int C, int G, int W, const float* beacons,
+                      const int32_t* counts, const float* cos_t, const float* sin_t,
+                      const void* qwin_block, double* Y, int32_t* row_slot) {
+    float* tmp = (float*)malloc(sizeof(float) * (size_t)D);
+    if (!tmp) return -2;
+    int r = 0;
+    for (int c = 0; c < C; ++c) {
+        if (counts[c] <= 0) continue;
+        orc_rope_row(D, beacons + (size_t)c * D, cos_t, sin_t, dtype == ORC_BF16, tmp);
+        for (int d = 0; d < D; ++d) Y[(size_t)r * D + d] = (double)tmp[d];
+        row_slot[r++] = c;
+    }
+    for (int g = 0; g < G; ++g) {
+        for (int w = 0; w < W; ++w) {
+            for (int d = 0; d < D; ++d)
+                Y[(size_t)r * D + d] = elem(qwin_block, ((size_t)g * W + w) * D + d, dtype);
+            row_slot[r++] = C + g * W + w;
+        }
+    }
+    free(tmp);
+    return r;
+}
+
+/* ---- (a3) scores -------------------------------------------------------------
+ *
+ * Attention weight of observation row r on cached key j (Eq. 4):
+ *   w_rj = exp(l_rj) / sum_l exp(l_rl),   l_rj = scale * <y_r, k_j>,
+ * normalised over all N cached keys.  The key score is the max of w_rj over
+ * every observation row, i.e. over all queries and all heads of the GQA group
+ * (Eq. 6, max form; Section 4.3 "Importance Scoring via Max-Aggregation";
+ * Algorithm 2, the Score step).  It is kept in the log domain:
+ *   lse_r = m_r + ln sum_j exp(l_rj - m_r),   m_r = max_j l_rj,
+ *   s_j   = max_r (l_rj - lse_r),  so exp(s_j) = max_r w_rj.
+ * With no rows at all every s_j is -inf.
+ * ------------------------------------------------------------------------ */
+int orc_score(int R, int N, int D, const double* Y, const void* Khead, int dtype, double scale,
+              double* lse, double* s) {
+    if (R == 0) {
+        for (int j = 0; j < N; ++j) s[j] = -INFINITY;
+        return 0;
+    }
+    double* logit = (double*)malloc(sizeof(double) * (size_t)R * (size_t)(N > 0 ? N : 1));
+    double* krow = (double*)malloc(sizeof(double) * (size_t)D);
+    if (!logit || !krow) {
+        free(logit);
+        free(krow);
+        return -2;
+    }
+    for (int j = 0; j < N; ++j) {
+        for (int d = 0; d < D; ++d) krow[d] = elem(Khead, (size_t)j * D + d, dtype);
+        for (int r = 0; r < R; ++r) {
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d) dot += Y[(size_t)r * D + d] * krow[d];
+            logit[(size_t)r * N + j] = scale * dot;
+        }
+    }
+    for (int r = 0; r < R; ++r) {
+        const double* l = logit + (size_t)r * N;
+        double m = -INFINITY;
+        for (int j = 0; j < N; ++j)
+            if (l[j] > m) m = l[j];
+        double z = 0.0;
+        for (int j = 0; j < N; ++j) z += exp(l[j] - m);
+        lse[r] = (N > 0) ? m + log(z) : -INFINITY;
+    }
+    for (int j = 0; j < N; ++j) {
+        double best = -INFINITY;
+        for (int r = 0; r < R; ++r) {
+            double v = logit[(size_t)r * N + j] - lse[r];
+            if (v > best) best = v;
+        }
+        s[j] = best;
+    }
+    free(logit);
+    free(krow);
+    return 0;
+}
+
+/* Score one kv-head from raw inputs: rows (a2) then (a3).  lse_slot is
+ * indexed by slot (C beacon slots, then G*W recent rows); empty beacon
+ * slots read -inf. */
+int orc_score_head(int dtype, int D, int N, int C, int G, int W, const void* Khead,
+                   const void* qwin_block, const float* beacons, const int32_t* counts,
+                   const float* cos_t, const float* sin_t, float scale, double* lse_slot,
+                   double* s) {
+    int Rmax = C + G * W;
+    double* Y = (double*)malloc(sizeof(double) * (size_t)(Rmax > 0 ? Rmax : 1) * D);
+    int32_t* slot = (int32_t*)malloc(sizeof(int32_t) * (size_t)(Rmax > 0 ? Rmax : 1));
+    double* lse = (double*)malloc(sizeof(double) * (size_t)(Rmax > 0 ? Rmax : 1));
+    if (!Y || !slot || !lse) {
+        free(Y);
+        free(slot);
+        free(lse);
+        return -2;
+    }
+    int R = orc_assemble_rows(dtype, D, C, G, W, beacons, counts, cos_t, sin_t, qwin_block, Y, slot);
+    double sc = (scale == 0.0f) ? (double)(float)(1.0 / sqrt((double)D)) : (double)scale;
+    int rc = orc_score(R, N, D, Y, Khead, dtype, sc, lse, s);
+    for (int i = 0; i < Rmax; ++i) lse_slot[i] = -INFINITY;
+    for (int r = 0; r < R; ++r) lse_slot[slot[r]] = lse[r];
+    free(Y);
+    free(slot);
+    free(lse);
+    return rc;
+}
+
+/* ---- (a4) selection -------------------------------------------------------
+ *
+ * Forced keep = the first n_prefix tokens and the last W tokens; the rest of
+ * the budget, k_sel = budget - |forced|, goes to the best-scoring other
+ * tokens, and the result is sorted (Section 2.2 TopK; Algorithm 2, the
+ * I_keep / k_sel / TopK / Sort steps).  "Best" is the order (score
+ * descending, index ascending): ties go to the lower index.  If N <= budget
+ * every token is kept.  Returns the number kept, min(budget, N).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+    double s;
+    int32_t idx;
+} orc_cand;
+
+static int orc_cand_cmp(const void* pa, const void* pb) {
+    const orc_cand* a = (const orc_cand*)pa;
+    const orc_cand* b = (const orc_cand*)pb;
+    if (a->s > b->s) return -1;
+    if (a->s < b->s) return 1;
+    return (a->idx > b->idx) - (a->idx < b->idx);
+}
+
+int orc_topk(int N, const double* s, int budget, int W, int n_prefix, int32_t* kept) {
+    if (N <= budget) {
+        for (int j = 0; j < N; ++j) kept[j] = j;
+        return N;
+    }
+    unsigned char* keep = (unsigned char*)calloc((size_t)N, 1);
+    orc_cand* cand = (orc_cand*)malloc(sizeof(orc_cand) * (size_t)N);
+    if (!keep || !cand) {
+        free(keep);
+        free(cand);
+        return -2;
+    }
+    int nforced = 0;
+    for (int j = 0; j < N; ++j) {
+        if (j < n_prefix || j >= N - W) {
+            keep[j] = 1;
+            ++nforced;
+        }
+    }
+    int ncand = 0;
+    for (int j = 0; j < N; ++j) {
+        if (!keep[j]) {
+            cand[ncand].s = s[j];
+            cand[ncand].idx = j;
+            ++ncand;
+        }
+    }
+    qsort(cand, (size_t)ncand, sizeof(orc_cand), orc_cand_cmp);
+    int ksel = budget - nforced;
+    for (int i = 0; i < ksel && i < ncand; ++i) keep[cand[i].idx] = 1;
+    int n = 0;
+    for (int j = 0; j < N; ++j)
+        if (keep[j]) kept[n++] = j;
+    free(keep);
+    free(cand);
+    return n;
+}
+
+/* ---- (a5) compaction ---------------------------------------------------
+ *
+ * Gather along the sequence axis, K^ = K[:, I, :] and V^ = V[:, I, :]
+ * (Section 2.2, Eq. 8; Algorithm 2, Gather after Sort).  Rows are copied
+ * bit for bit from a snapshot of the original head, so the in-place result
+ * equals the out-of-place gather.  Rows at n_keep and beyond are untouched.
+ * ------------------------------------------------------------------------ */
+int orc_compact(int esize, int D, int n_keep, const int32_t* kept, void* Khead, void* Vhead) {
+    size_t row = (size_t)esize * (size_t)D;
+    unsigned char* tk = (unsigned char*)malloc(row * (size_t)(n_keep > 0 ? n_keep : 1));
+    unsigned char* tv = (unsigned char*)malloc(row * (size_t)(n_keep > 0 ? n_keep : 1));
+    if (!tk || !tv) {
+        free(tk);
+        free(tv);
+        return -2;
+    }
+    for (int i = 0; i < n_keep; ++i) {
+        memcpy(tk + row * i, (unsigned char*)Khead + row * (size_t)kept[i], row);
+        memcpy(tv + row * i, (unsigned char*)Vhead + row * (size_t)kept[i], row);
+    }
+    memcpy(Khead, tk, row * (size_t)n_keep);
+    memcpy(Vhead, tv, row * (size_t)n_keep);
+    free(tk);
+    free(tv);
+    return 0;
+}
+
+/* ---- (a6) the whole eviction of one kv-head: (a2) -> (a3) -> (a4) -> (a5).
+ * Returns the number of rows kept (or a negative error). */
+int orc_evict_head(int dtype, int D, int N, int C, int G, int W, int budget, int n_prefix,
+                   void* Khead, void* Vhead, const void* qwin_block, const float* beacons,
+                   const int32_t* counts, const float* cos_t, const float* sin_t, float scale,
+                   double* lse_slot, double* s, int32_t* kept) {
+    int rc = orc_score_head(dtype, D, N, C, G, W, Khead, qwin_block, beacons, counts, cos_t,
+                            sin_t, scale, lse_slot, s);
+    if (rc) return rc;
+    int n = orc_topk(N, s, budget, W, n_prefix, kept);
+    if (n < 0) return n;
+    rc = orc_compact(dtype == ORC_BF16 ? 2 : 4, D, n, kept, Khead, Vhead);
+    return rc ? rc : n;
+}
