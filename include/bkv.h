@@ -1,0 +1,182 @@
+/*
+ * bkv.h -- C ABI of the BeaconKV eviction step on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "BeaconKV: Key-Value Cache Compression Guided by Beacon Queries for
+ * Efficient Large Reasoning Model Inference" (arXiv 2609.04971).
+ *
+ * One KV-cache layer is evicted per call, every (batch, kv-head) pair
+ * independently.  Notation: P = B*Hkv heads, G = Hq/Hkv query heads per
+ * kv-head, and query head hq belongs to kv-head hq / G (contiguous GQA
+ * grouping).  All layouts are dense row-major with the last dimension
+ * contiguous:
+ *
+ *   K, V      [B, Hkv, N_cap, D]  cache (post-RoPE keys), dtype of the dims
+ *   q_new     [B, Hq,  T,     D]  newest pre-RoPE queries, dtype of the dims
+ *   q_win     [B, Hq,  W,     D]  recent queries, already rotated at their own
+ *                                 positions, dtype of the dims; any order
+ *   beacons   [B, Hkv, C,     D]  fp32 beacon vectors (pre-RoPE)
+ *   counts    [B, Hkv, C]         int32 members per beacon; 0 = empty slot
+ *   rope_cos, rope_sin [D/2]      fp32 rotation table for the current step
+ *   scores    [B, Hkv, N]         fp32 log-domain key scores
+ *   row_lse   [B, Hkv, C + G*W]   fp32 per-row log-normaliser, slot-indexed
+ *   kept      [B, Hkv, min(budget, N)]  int32 kept token indices, ascending
+ *
+ * Conventions for every entry point:
+ *   - Pointers to tensors are device pointers owned by the caller.  The
+ *     library allocates nothing; scratch comes from the caller's workspace.
+ *   - Work is enqueued on `stream` and is asynchronous; no call synchronises
+ *     except bkv_device_status.
+ *   - Arguments are validated on the host before anything is enqueued; on an
+ *     error no work is enqueued and no buffer changes.  Launch failures map to
+ *     BKV_ERR_HIP.
+ *   - Inputs must be finite.  Non-finite values give an unspecified ranking,
+ *     but never an out-of-bounds access and always an exact kept count.
+ *   - Calls that share a workspace must be ordered on one stream.
+ */
+#ifndef BKV_H
+#define BKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BKV_OK = 0,
+    BKV_ERR_INVALID = 1,   /* NULL pointer or value out of range */
+    BKV_ERR_SHAPE = 2,     /* inconsistent or unsupported dimensions */
+    BKV_ERR_DTYPE = 3,     /* unsupported element type */
+    BKV_ERR_WORKSPACE = 4, /* workspace missing, too small or not initialised */
+    BKV_ERR_HIP = 5,       /* a HIP runtime call failed */
+    BKV_ERR_DEVICE = 6     /* a device-side check tripped (see bkv_device_status) */
+} bkv_status;
+
+typedef enum { BKV_F32 = 0, BKV_BF16 = 1 } bkv_dtype;
+
+typedef enum {
+    BKV_OP_BEACON_UPDATE = 0,
+    BKV_OP_SCORE = 1,
+    BKV_OP_TOPK = 2,
+    BKV_OP_COMPACT = 3,
+    BKV_OP_EVICT = 4
+} bkv_op;
+
+typedef struct {
+    int32_t B;        /* batch, >= 0 (0 makes every call a no-op) */
+    int32_t Hq;       /* query heads, a positive multiple of Hkv */
+    int32_t Hkv;      /* kv heads, >= 1 */
+    int32_t D;        /* head dimension, 64 or 128 */
+    int32_t N;        /* valid cached tokens per head, 0 <= N <= N_cap */
+    int32_t N_cap;    /* allocated tokens per head: the head stride of K and V */
+    int32_t W;        /* recent queries per query head, and recent tokens always kept */
+    int32_t C;        /* beacon slots per kv-head, 0..64 */
+    int32_t budget;   /* tokens kept per kv-head (B_KV^min), >= max(1, W + n_prefix) */
+    int32_t n_prefix; /* leading tokens always kept, counted inside the budget */
+    int32_t dtype;    /* bkv_dtype of K, V, q_new and q_win */
+} bkv_dims;
+
+/* Host-only check of `d` for operation `op` (a bkv_op).  Enqueues nothing.
+ * Rules: Hkv >= 1, Hq % Hkv == 0, D in {64, 128}, 0 <= N <= N_cap,
+ * N_cap >= 1, W >= 0, 0 <= C <= 64, n_prefix >= 0,
+ * budget >= max(1, W + n_prefix), dtype in {BKV_F32, BKV_BF16};
+ * scoring (SCORE, EVICT) also needs 1 <= C + G*W <= 1024; the beacon
+ * update needs C >= 1. */
+bkv_status bkv_validate(const bkv_dims* d, int32_t op);
+
+/* Bytes of workspace `op` needs for `d` (0 when it needs none).  One
+ * workspace sized for BKV_OP_EVICT serves every operation on those dims. */
+size_t bkv_workspace_bytes(const bkv_dims* d, int32_t op);
+
+/* Enqueue the initialisation of a workspace: clears its control block and
+ * stamps it with (B*Hkv, budget).  Required once after allocation, again
+ * whenever B*Hkv or budget change, and after a BKV_ERR_DEVICE.  Kernels
+ * leave the control block clear when they finish, so calls in between need
+ * nothing.  A kernel that finds a workspace not stamped for its dims does no
+ * work and raises BKV_ERR_DEVICE. */
+bkv_status bkv_workspace_init(const bkv_dims* d, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Synchronise `stream`, then report the device-side error word of `ws`:
+ * BKV_OK, or BKV_ERR_DEVICE if a bounded wait timed out or the workspace
+ * stamp did not match (the affected outputs are then unspecified). */
+bkv_status bkv_device_status(const void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* (a1) Beacon maintenance.  For each (b, kv-head), the T*G new pre-RoPE
+ * queries of its query heads are taken in order t-major, then g ascending.
+ * Each one fills the lowest empty slot if there is one (count 1); otherwise
+ * it joins the slot of largest cosine similarity (ties -> lowest slot;
+ * cosine 0 when a norm is 0), whose count grows by one and whose vector
+ * moves to the running mean: beta += (x - beta) / count.  Beacons represent
+ * clusters of pre-RoPE queries under cosine similarity (Section 3.2,
+ * "Beacon queries"; Section 4.2; Appendix D.1, the nearest-representative
+ * similarity of Algorithm 1).
+ *   q_new   [B,Hq,T,D] read;  beacons, counts  read and written in place.
+ *   assign  optional [B,Hkv,T*G] int32 output: the slot each query joined,
+ *           in processing order; NULL to skip.
+ *   T >= 0 (0 is a no-op).  Needs no workspace. */
+bkv_status bkv_beacon_update(const bkv_dims* d, const void* q_new, int32_t T, float* beacons,
+                             int32_t* counts, int32_t* assign, hipStream_t stream);
+
+/* (a2)+(a3) Scores.  Per (b, kv-head) the observation rows are: every
+ * occupied beacon slot c in ascending order, rotated to the current step
+ * with rotate-half RoPE (pair (i, i+D/2) turned by rope_cos[i], rope_sin[i];
+ * products rounded to fp32, then the sum, no fused multiply-add) and then
+ * rounded to the cache dtype (bf16: nearest-even); then the G*W recent
+ * queries as given (Section 4.3, "Query Construction and Alignment";
+ * Algorithm 2, the union of beacon and recent queries).  Both tables NULL
+ * means no rotation.  With l_rj = scale * <y_r, k_j> (fp32 accumulation;
+ * scale 0 selects fp32(1/sqrt(D))), every row is normalised over all N keys
+ * (Eq. 4) and the key score is the max over rows (Eq. 6, max form;
+ * Section 4.3 "Importance Scoring via Max-Aggregation"):
+ *   lse_r = log sum_j exp(l_rj),   scores[j] = max_r (l_rj - lse_r) <= 0,
+ * so exp(scores[j]) is the largest attention weight key j receives.  With
+ * no occupied slot and W == 0 every score is -inf.
+ *   row_lse optional (NULL to skip): entry c for beacon slot c (-inf when
+ *           empty), entry C + g*W + w for recent query w of head h*G+g.
+ *   N == 0: nothing is written.  Workspace: bkv_workspace_bytes(d, SCORE). */
+bkv_status bkv_score(const bkv_dims* d, const void* K, const void* q_win, const float* beacons,
+                     const int32_t* counts, const float* rope_cos, const float* rope_sin,
+                     float scale, float* scores, float* row_lse, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* (a4) Selection.  If N <= budget, kept = 0..N-1.  Otherwise the first
+ * n_prefix and the last W tokens are always kept and the remaining
+ * budget - n_prefix - W places go to the other tokens of highest score,
+ * ties to the lower index (-0 equals +0); kept is emitted in ascending
+ * order (Section 2.2 TopK; Algorithm 2, the I_keep, k_sel, TopK and Sort
+ * steps).  scores [B,Hkv,N] read; kept [B,Hkv,min(budget,N)] written.
+ * Needs no workspace (ws may be NULL). */
+bkv_status bkv_topk(const bkv_dims* d, const float* scores, int32_t* kept, void* ws,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* (a5) In-place, order-preserving compaction: for i < n = min(budget, N),
+ * row i of K and of V becomes original row kept[i] (Section 2.2, Eq. 8;
+ * Algorithm 2, Gather after Sort), bit for bit.  kept must be strictly
+ * ascending within [0, N) per head (as bkv_topk emits); rows from n on are
+ * left as they were.  Workspace: bkv_workspace_bytes(d, COMPACT). */
+bkv_status bkv_compact(const bkv_dims* d, void* K, void* V, const int32_t* kept, void* ws,
+                       size_t ws_bytes, hipStream_t stream);
+
+/* (a6) The whole eviction of one layer: bkv_score, bkv_topk, bkv_compact in
+ * order on `stream`.  scores, row_lse and kept are optional outputs (NULL:
+ * scores and kept live in the workspace).  Afterwards each head holds
+ * min(budget, N) rows.  Workspace: bkv_workspace_bytes(d, EVICT). */
+bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, const float* beacons,
+                     const int32_t* counts, const float* rope_cos, const float* rope_sin,
+                     float scale, int32_t* kept, float* scores, float* row_lse, void* ws,
+                     size_t ws_bytes, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* bkv_status_string(bkv_status s);
+
+/* ABI version of this header, 1. */
+int32_t bkv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BKV_H */

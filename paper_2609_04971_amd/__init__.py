@@ -1,0 +1,242 @@
+"""Python binding of libbkv.so, the MI355X (gfx950) BeaconKV eviction step.
+
+Argument marshalling only: every step of the path runs in the HIP kernels
+behind include/bkv.h.  torch supplies device memory and the stream (work is
+enqueued on torch's current stream).  Tensor shapes, dtypes, devices and
+contiguity are checked here because the C ABI takes bare pointers and
+cannot see them.  There is no fallback: if the library is not built this
+module fails to import.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libbkv.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_04971_amd.build`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+OK, ERR_INVALID, ERR_SHAPE, ERR_DTYPE, ERR_WORKSPACE, ERR_HIP, ERR_DEVICE = range(7)
+F32, BF16 = 0, 1
+OP_BEACON_UPDATE, OP_SCORE, OP_TOPK, OP_COMPACT, OP_EVICT = range(5)
+
+EXPORTS = ("bkv_validate", "bkv_workspace_bytes", "bkv_workspace_init", "bkv_device_status",
+           "bkv_beacon_update", "bkv_score", "bkv_topk", "bkv_compact", "bkv_evict",
+           "bkv_status_string", "bkv_abi_version")
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("B", "Hq", "Hkv", "D", "N", "N_cap", "W", "C", "budget", "n_prefix", "dtype")]
+
+    @property
+    def G(self):
+        return self.Hq // self.Hkv
+
+    @property
+    def P(self):
+        return self.B * self.Hkv
+
+    @property
+    def n_keep(self):
+        return min(self.budget, self.N)
+
+    def replace(self, **kw):
+        d = Dims()
+        for n, _ in self._fields_:
+            setattr(d, n, kw.get(n, getattr(self, n)))
+        return d
+
+    def __repr__(self):
+        return "Dims(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
+
+
+def dims(B, Hq, Hkv, D, N, W, C, budget, n_prefix=0, dtype="bf16", N_cap=None) -> Dims:
+    d = Dims()
+    d.B, d.Hq, d.Hkv, d.D, d.N = B, Hq, Hkv, D, N
+    d.N_cap = N if N_cap is None else N_cap
+    d.W, d.C, d.budget, d.n_prefix = W, C, budget, n_prefix
+    d.dtype = {"bf16": BF16, "fp32": F32, BF16: BF16, F32: F32}[dtype]
+    return d
+
+
+_P = ctypes.c_void_p
+_D = ctypes.POINTER(Dims)
+_S = ctypes.c_size_t
+_lib.bkv_validate.argtypes = [_D, ctypes.c_int32]
+_lib.bkv_validate.restype = ctypes.c_int
+_lib.bkv_workspace_bytes.argtypes = [_D, ctypes.c_int32]
+_lib.bkv_workspace_bytes.restype = _S
+_lib.bkv_workspace_init.argtypes = [_D, _P, _S, _P]
+_lib.bkv_workspace_init.restype = ctypes.c_int
+_lib.bkv_device_status.argtypes = [_P, _S, _P]
+_lib.bkv_device_status.restype = ctypes.c_int
+_lib.bkv_beacon_update.argtypes = [_D, _P, ctypes.c_int32, _P, _P, _P, _P]
+_lib.bkv_beacon_update.restype = ctypes.c_int
+_lib.bkv_score.argtypes = [_D, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _S, _P]
+_lib.bkv_score.restype = ctypes.c_int
+_lib.bkv_topk.argtypes = [_D, _P, _P, _P, _S, _P]
+_lib.bkv_topk.restype = ctypes.c_int
+_lib.bkv_compact.argtypes = [_D, _P, _P, _P, _P, _S, _P]
+_lib.bkv_compact.restype = ctypes.c_int
+_lib.bkv_evict.argtypes = [_D, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P]
+_lib.bkv_evict.restype = ctypes.c_int
+_lib.bkv_status_string.argtypes = [ctypes.c_int]
+_lib.bkv_status_string.restype = ctypes.c_char_p
+_lib.bkv_abi_version.argtypes = []
+_lib.bkv_abi_version.restype = ctypes.c_int32
+
+
+class BkvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+def status_string(st: int) -> str:
+    return _lib.bkv_status_string(st).decode()
+
+
+def abi_version() -> int:
+    return int(_lib.bkv_abi_version())
+
+
+def _check(st: int, where: str):
+    if st != OK:
+        raise BkvError(st, where)
+
+
+def validate(d: Dims, op: int) -> int:
+    """Host-only validation (no GPU needed); returns the bkv_status code."""
+    return int(_lib.bkv_validate(ctypes.byref(d), op))
+
+
+def workspace_bytes(d: Dims, op: int = OP_EVICT) -> int:
+    return int(_lib.bkv_workspace_bytes(ctypes.byref(d), op))
+
+
+# ---- marshalling helpers ---------------------------------------------------
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _tdtype(d: Dims):
+    return torch.bfloat16 if d.dtype == BF16 else torch.float32
+
+
+def _ptr(t, shape=None, dtype=None, name="tensor", optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _ws(ws):
+    if ws is None:
+        return None, 0
+    if not isinstance(ws, torch.Tensor) or ws.device.type != "cuda" or not ws.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
+    return ctypes.c_void_p(ws.data_ptr()), ws.numel() * ws.element_size()
+
+
+# ---- workspace -----------------------------------------------------------------
+def workspace(d: Dims, op: int = OP_EVICT, device="cuda") -> torch.Tensor:
+    """Allocate (through torch) and initialise a workspace for `op` on `d`."""
+    n = workspace_bytes(d, op)
+    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+    workspace_init(d, ws)
+    return ws
+
+
+def workspace_init(d: Dims, ws: torch.Tensor):
+    p, n = _ws(ws)
+    _check(_lib.bkv_workspace_init(ctypes.byref(d), p, n, _stream()), "bkv_workspace_init")
+
+
+def device_status(ws: torch.Tensor) -> int:
+    """Synchronise the current stream and return the workspace's device status."""
+    p, n = _ws(ws)
+    return int(_lib.bkv_device_status(p, n, _stream()))
+
+
+# ---- operations ------------------------------------------------------------------
+def beacon_update(d: Dims, q_new, beacons, counts, assign=None):
+    """(a1) in place on beacons [B,Hkv,C,D] fp32 and counts [B,Hkv,C] int32."""
+    T = q_new.shape[2]
+    st = _lib.bkv_beacon_update(
+        ctypes.byref(d), _ptr(q_new, (d.B, d.Hq, T, d.D), _tdtype(d), "q_new"), T,
+        _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
+        _ptr(counts, (d.B, d.Hkv, d.C), torch.int32, "counts"),
+        _ptr(assign, (d.B, d.Hkv, T * d.G), torch.int32, "assign", optional=True), _stream())
+    _check(st, "bkv_beacon_update")
+
+
+def _rope(rope_cos, rope_sin, d):
+    return (_ptr(rope_cos, (d.D // 2,), torch.float32, "rope_cos", optional=True),
+            _ptr(rope_sin, (d.D // 2,), torch.float32, "rope_sin", optional=True))
+
+
+def score(d: Dims, K, q_win, beacons, counts, scores, ws, row_lse=None, rope_cos=None, rope_sin=None,
+          scale: float = 0.0):
+    """(a2)+(a3): scores [B,Hkv,N] fp32 (and row_lse [B,Hkv,C+G*W]) written."""
+    rc, rs = _rope(rope_cos, rope_sin, d)
+    wp, wn = _ws(ws)
+    st = _lib.bkv_score(
+        ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+        _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),
+        _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
+        _ptr(counts, (d.B, d.Hkv, d.C), torch.int32, "counts"), rc, rs, float(scale),
+        _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores"),
+        _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True), wp, wn,
+        _stream())
+    _check(st, "bkv_score")
+
+
+def topk(d: Dims, scores, kept, ws=None):
+    """(a4): kept [B,Hkv,min(budget,N)] int32 written, ascending."""
+    wp, wn = _ws(ws)
+    st = _lib.bkv_topk(ctypes.byref(d), _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores"),
+                       _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept"), wp, wn, _stream())
+    _check(st, "bkv_topk")
+
+
+def compact(d: Dims, K, V, kept, ws):
+    """(a5): rows i < n of K and V become rows kept[i], in place."""
+    wp, wn = _ws(ws)
+    st = _lib.bkv_compact(ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+                          _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
+                          _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept"), wp, wn, _stream())
+    _check(st, "bkv_compact")
+
+
+def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row_lse=None, rope_cos=None,
+          rope_sin=None, scale: float = 0.0):
+    """(a6): score -> select -> compact one layer in place."""
+    rc, rs = _rope(rope_cos, rope_sin, d)
+    wp, wn = _ws(ws)
+    st = _lib.bkv_evict(
+        ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+        _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
+        _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),
+        _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
+        _ptr(counts, (d.B, d.Hkv, d.C), torch.int32, "counts"), rc, rs, float(scale),
+        _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept", optional=True),
+        _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores", optional=True),
+        _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True), wp, wn,
+        _stream())
+    _check(st, "bkv_evict")

@@ -1,0 +1,246 @@
+// C ABI of the eviction-step library (declared in include/bkv.h): host-side
+// validation, workspace layout, and the enqueue of each operation's kernels.
+// Nothing here allocates device memory or synchronises, except
+// bkv_device_status, which is documented to.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "bkv.h"
+#include "internal.h"
+
+namespace bkv {
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+constexpr int kMaxRows = 1024;  // observation rows per head (C + G*W)
+constexpr int kMaxC = 64;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+__global__ void ws_init_kernel(int* ws, int nwords, int P, int budget) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < nwords; i += gridDim.x * blockDim.x) {
+        int v = 0;
+        if (i == kHdrMagic) v = (int)kWsMagic;
+        if (i == kHdrP) v = P;
+        if (i == kHdrBudget) v = budget;
+        ws[i] = v;
+    }
+}
+
+}  // namespace
+
+WsLayout ws_layout(const bkv_dims& d) {
+    WsLayout L;
+    memset(&L, 0, sizeof L);
+    const int P = d.B * d.Hkv;
+    const int G = d.Hkv > 0 ? d.Hq / d.Hkv : 0;
+    L.P = P;
+    L.nseg = (d.budget + kSegRows - 1) / kSegRows;
+    const size_t es = d.dtype == BKV_BF16 ? 2 : 4;
+    size_t off = kHdrWords * sizeof(int);
+    L.ready0 = off;
+    off = align_up(off + sizeof(int) * (size_t)P);
+    L.p1cnt = off;
+    off = align_up(off + sizeof(int) * (size_t)P);
+    L.ready = off;
+    off = align_up(off + sizeof(int) * (size_t)P);
+    L.cflags = off;
+    off = align_up(off + sizeof(int) * (size_t)P * L.nseg);
+    L.ctl_end = off;
+    // data (depends on N, W, C as well)
+    const int R = d.C + G * d.W;
+    L.R_pad_max = (R + 15) / 16 * 16;
+    // key chunk per score work item: 1024 keys once there are enough chunks
+    // to fill the machine several times over, else 256
+    const long long big = (long long)P * ((d.N + 1023) / 1024);
+    L.kgn = big >= 2048 ? 4 : 1;
+    L.key_chunk = 256 * L.kgn;
+    L.nch = (d.N + L.key_chunk - 1) / L.key_chunk;
+    L.Y = off;
+    off = align_up(off + es * (size_t)P * L.R_pad_max * d.D);
+    L.rowslot = off;
+    off = align_up(off + sizeof(int) * (size_t)P * L.R_pad_max);
+    L.ract = off;
+    off = align_up(off + sizeof(int) * (size_t)P);
+    L.partials = off;
+    off = align_up(off + 2 * sizeof(float) * (size_t)P * L.nch * L.R_pad_max);
+    L.lse2 = off;
+    off = align_up(off + sizeof(float) * (size_t)P * L.R_pad_max);
+    L.score_end = off;
+    L.scores = off;
+    off = align_up(off + sizeof(float) * (size_t)P * d.N);
+    L.kept = off;
+    off = align_up(off + sizeof(int32_t) * (size_t)P * d.budget);
+    L.evict_end = off;
+    return L;
+}
+
+}  // namespace bkv
+
+using namespace bkv;
+
+namespace {
+
+bkv_status map_hip(hipError_t e) { return e == hipSuccess ? BKV_OK : BKV_ERR_HIP; }
+
+bool empty_batch(const bkv_dims* d) { return d->B == 0; }
+
+}  // namespace
+
+extern "C" {
+
+bkv_status bkv_validate(const bkv_dims* d, int32_t op) {
+    if (!d) return BKV_ERR_INVALID;
+    if (op < BKV_OP_BEACON_UPDATE || op > BKV_OP_EVICT) return BKV_ERR_INVALID;
+    if (d->dtype != BKV_F32 && d->dtype != BKV_BF16) return BKV_ERR_DTYPE;
+    if (d->B < 0 || d->Hkv < 1 || d->Hq < 1 || d->Hq % d->Hkv != 0) return BKV_ERR_SHAPE;
+    if (d->D != 64 && d->D != 128) return BKV_ERR_SHAPE;
+    if (d->N_cap < 1 || d->N < 0 || d->N > d->N_cap) return BKV_ERR_SHAPE;
+    if (d->W < 0 || d->C < 0 || d->C > kMaxC || d->n_prefix < 0) return BKV_ERR_SHAPE;
+    if ((long long)d->W + d->n_prefix > d->budget || d->budget < 1) return BKV_ERR_SHAPE;
+    const long long G = d->Hq / d->Hkv;
+    // index arithmetic stays in 32 bits where the kernels use int
+    if ((long long)d->B * d->Hkv * d->N_cap > 0x7fffffffLL || (long long)d->B * d->Hq * d->W > 0x7fffffffLL)
+        return BKV_ERR_SHAPE;
+    if (op == BKV_OP_SCORE || op == BKV_OP_EVICT) {
+        const long long R = d->C + G * d->W;
+        if (R < 1 || R > kMaxRows) return BKV_ERR_SHAPE;
+    }
+    if (op == BKV_OP_BEACON_UPDATE && d->C < 1) return BKV_ERR_SHAPE;
+    return BKV_OK;
+}
+
+size_t bkv_workspace_bytes(const bkv_dims* d, int32_t op) {
+    if (bkv_validate(d, op) != BKV_OK) return 0;
+    const WsLayout L = ws_layout(*d);
+    switch (op) {
+        case BKV_OP_SCORE: return L.score_end;
+        case BKV_OP_COMPACT: return L.ctl_end;
+        case BKV_OP_EVICT: return L.evict_end;
+        default: return 0;
+    }
+}
+
+bkv_status bkv_workspace_init(const bkv_dims* d, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!d || !ws) return BKV_ERR_INVALID;
+    bkv_status st = bkv_validate(d, BKV_OP_COMPACT);
+    if (st != BKV_OK) return st;
+    const WsLayout L = ws_layout(*d);
+    if (ws_bytes < L.ctl_end) return BKV_ERR_WORKSPACE;
+    const int nwords = (int)(L.ctl_end / sizeof(int));
+    int blocks = (nwords + 255) / 256;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(ws_init_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<int*>(ws), nwords, L.P,
+                       d->budget);
+    return map_hip(hipGetLastError());
+}
+
+bkv_status bkv_device_status(const void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!ws || ws_bytes < kHdrWords * sizeof(int)) return BKV_ERR_INVALID;
+    if (hipStreamSynchronize(stream) != hipSuccess) return BKV_ERR_HIP;
+    int hdr[4];
+    if (hipMemcpy(hdr, ws, sizeof hdr, hipMemcpyDeviceToHost) != hipSuccess) return BKV_ERR_HIP;
+    if ((uint32_t)hdr[kHdrMagic] != kWsMagic) return BKV_ERR_WORKSPACE;
+    return hdr[kHdrErr] ? BKV_ERR_DEVICE : BKV_OK;
+}
+
+bkv_status bkv_beacon_update(const bkv_dims* d, const void* q_new, int32_t T, float* beacons, int32_t* counts,
+                             int32_t* assign, hipStream_t stream) {
+    bkv_status st = bkv_validate(d, BKV_OP_BEACON_UPDATE);
+    if (st != BKV_OK) return st;
+    if (T < 0) return BKV_ERR_SHAPE;
+    if (empty_batch(d) || T == 0) return BKV_OK;
+    if (!q_new || !beacons || !counts) return BKV_ERR_INVALID;
+    if ((long long)d->B * d->Hq * T * d->D > 0x7fffffffLL) return BKV_ERR_SHAPE;
+    return map_hip(launch_beacon_update(*d, q_new, T, beacons, counts, assign, stream));
+}
+
+static bkv_status check_score_args(const bkv_dims* d, const void* K, const void* q_win, const float* beacons,
+                                   const int32_t* counts, const float* rope_cos, const float* rope_sin,
+                                   float scale) {
+    if (!K || ((!beacons || !counts) && d->C > 0) || (!q_win && d->W > 0)) return BKV_ERR_INVALID;
+    if ((rope_cos == nullptr) != (rope_sin == nullptr)) return BKV_ERR_INVALID;
+    if (!aligned16(K) || (q_win && !aligned16(q_win))) return BKV_ERR_INVALID;
+    if (!(scale >= 0.0f) || isinf(scale)) return BKV_ERR_INVALID;
+    return BKV_OK;
+}
+
+bkv_status bkv_score(const bkv_dims* d, const void* K, const void* q_win, const float* beacons,
+                     const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
+                     float* scores, float* row_lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+    bkv_status st = bkv_validate(d, BKV_OP_SCORE);
+    if (st != BKV_OK) return st;
+    if (empty_batch(d) || d->N == 0) return BKV_OK;
+    st = check_score_args(d, K, q_win, beacons, counts, rope_cos, rope_sin, scale);
+    if (st != BKV_OK) return st;
+    if (!scores) return BKV_ERR_INVALID;
+    const WsLayout L = ws_layout(*d);
+    if (!ws || ws_bytes < L.score_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
+    return map_hip(launch_score(*d, L, K, q_win, beacons, counts, rope_cos, rope_sin, scale, scores, row_lse, ws,
+                                stream));
+}
+
+bkv_status bkv_topk(const bkv_dims* d, const float* scores, int32_t* kept, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
+    (void)ws;
+    (void)ws_bytes;
+    bkv_status st = bkv_validate(d, BKV_OP_TOPK);
+    if (st != BKV_OK) return st;
+    if (empty_batch(d) || d->N == 0) return BKV_OK;
+    if (!scores || !kept) return BKV_ERR_INVALID;
+    return map_hip(launch_topk(*d, scores, kept, stream));
+}
+
+bkv_status bkv_compact(const bkv_dims* d, void* K, void* V, const int32_t* kept, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+    bkv_status st = bkv_validate(d, BKV_OP_COMPACT);
+    if (st != BKV_OK) return st;
+    if (empty_batch(d) || d->N == 0) return BKV_OK;
+    if (!K || !V || !kept) return BKV_ERR_INVALID;
+    if (!aligned16(K) || !aligned16(V)) return BKV_ERR_INVALID;
+    const WsLayout L = ws_layout(*d);
+    if (!ws || ws_bytes < L.ctl_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
+    return map_hip(launch_compact(*d, L, K, V, kept, ws, stream));
+}
+
+bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, const float* beacons,
+                     const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
+                     int32_t* kept, float* scores, float* row_lse, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+    bkv_status st = bkv_validate(d, BKV_OP_EVICT);
+    if (st != BKV_OK) return st;
+    if (empty_batch(d) || d->N == 0) return BKV_OK;
+    st = check_score_args(d, K, q_win, beacons, counts, rope_cos, rope_sin, scale);
+    if (st != BKV_OK) return st;
+    if (!V || !aligned16(V)) return BKV_ERR_INVALID;
+    const WsLayout L = ws_layout(*d);
+    if (!ws || ws_bytes < L.evict_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
+    char* w = static_cast<char*>(ws);
+    float* sc = scores ? scores : reinterpret_cast<float*>(w + L.scores);
+    int32_t* kp = kept ? kept : reinterpret_cast<int32_t*>(w + L.kept);
+    hipError_t e = launch_score(*d, L, K, q_win, beacons, counts, rope_cos, rope_sin, scale, sc, row_lse, ws, stream);
+    if (e != hipSuccess) return BKV_ERR_HIP;
+    e = launch_topk(*d, sc, kp, stream);
+    if (e != hipSuccess) return BKV_ERR_HIP;
+    return map_hip(launch_compact(*d, L, K, V, kp, ws, stream));
+}
+
+const char* bkv_status_string(bkv_status s) {
+    switch (s) {
+        case BKV_OK: return "ok";
+        case BKV_ERR_INVALID: return "invalid argument";
+        case BKV_ERR_SHAPE: return "invalid or unsupported shape";
+        case BKV_ERR_DTYPE: return "unsupported dtype";
+        case BKV_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+        case BKV_ERR_HIP: return "HIP runtime error";
+        case BKV_ERR_DEVICE: return "device-side check failed";
+    }
+    return "unknown status";
+}
+
+int32_t bkv_abi_version(void) { return 1; }
+
+}  // extern "C"

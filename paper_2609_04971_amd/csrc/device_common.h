@@ -1,0 +1,84 @@
+// Device helpers shared by the gfx950 kernels: scoped atomics, a bounded
+// wait, wave shuffles and bf16 rounding.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "internal.h"
+
+namespace bkv {
+namespace dev {
+
+// 16 bytes as a native vector: loads and stores of it are single 128-bit
+// memory instructions and it always stays in registers (a struct copy of
+// uint4 goes through memcpy and can end up in scratch).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Cross-workgroup hand-offs use agent-scope acquire/release: the MI355X's
+// eight XCDs have separate L2 caches, and agent scope is what makes a
+// release on one XCD visible to an acquire on another.
+__device__ inline int ld_acquire(const int* p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void st_release(int* p, int v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline int fetch_add_acq_rel(int* p, int v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline int fetch_add_relaxed(int* p, int v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void raise_error(int* hdr, int bits) {
+    __hip_atomic_fetch_or(hdr + kHdrErr, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bounded wait for *p >= v.  Every wait in this library is on work with a
+// lower ticket, which has already started and never waits itself, so it
+// ends; the bound only turns a broken invariant into an error instead of a
+// hang.  About 2^22 polls with a short sleep between them.
+constexpr int kSpinLimit = 1 << 22;
+__device__ inline bool wait_geq(const int* p, int v) {
+    for (int i = 0; i < kSpinLimit; ++i) {
+        if (ld_acquire(p) >= v) return true;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return false;
+}
+
+// Compile-time loop: f(std::integral_constant<int, i>) for i = 0..N-1.
+// Keeps register arrays indexed by constants from the start, so they are
+// never demoted to scratch memory.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Workspace stamp check (one thread).
+__device__ inline bool stamp_ok(const int* hdr, int P, int budget) {
+    return (uint32_t)hdr[kHdrMagic] == kWsMagic && hdr[kHdrP] == P && hdr[kHdrBudget] == budget;
+}
+
+__device__ inline float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, 64); }
+__device__ inline int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, 64); }
+
+// bf16 <-> fp32.  bf16 is the top half of binary32; rounding is to
+// nearest, ties to even, and NaN stays NaN.
+__device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ inline uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+}  // namespace dev
+}  // namespace bkv

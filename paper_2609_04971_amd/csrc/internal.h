@@ -1,0 +1,71 @@
+// Internal interface between the C ABI (abi.hip) and the kernel files.
+// Not installed; the public contract is include/bkv.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "bkv.h"
+
+namespace bkv {
+
+// ---- workspace --------------------------------------------------------------
+// Control block (must be all-zero at rest except the stamp), then data.
+// The control block's size and offsets depend only on P = B*Hkv and budget,
+// so one initialised workspace stays valid while N, W or C change.
+constexpr uint32_t kWsMagic = 0x424b5631u;  // "BKV1"
+
+enum HdrWord : int {
+    kHdrMagic = 0,
+    kHdrP = 1,
+    kHdrBudget = 2,
+    kHdrErr = 3,        // sticky device error bits, cleared only by init
+    kHdrScTicket = 4,   // score kernel work ticket
+    kHdrScDone = 5,     // score kernel finished work items
+    kHdrCpTicket = 6,   // compaction kernel work ticket
+    kHdrCpDone = 7,     // compaction kernel finished work items
+    kHdrWords = 64      // header is 256 bytes
+};
+
+enum DevErr : int { kErrScoreWait = 1, kErrCompactWait = 2, kErrStamp = 4, kErrBadIndex = 8 };
+
+constexpr int kSegRows = 64;  // compaction rows per work item
+
+struct WsLayout {
+    // control block
+    size_t ready0, p1cnt, ready;  // score: per-head flags / counters (int32 [P])
+    size_t cflags;                // compaction: per-segment read-done flags (int32 [P][nseg])
+    size_t ctl_end;
+    // data
+    size_t Y;         // assembled observation rows [P][R_pad_max][D] of the cache dtype
+    size_t rowslot;   // slot id of every row [P][R_pad_max]
+    size_t ract;      // rows per head [P]
+    size_t partials;  // per-chunk row statistics (m, z) [P][nch][R_pad_max] float2
+    size_t lse2;      // row log2-normalisers [P][R_pad_max]
+    size_t score_end;
+    size_t scores;    // evict: scores when the caller passes none [P][N]
+    size_t kept;      // evict: kept indices when the caller passes none [P][budget]
+    size_t evict_end;
+    int P, nseg, R_pad_max, nch, kgn, key_chunk;
+};
+
+WsLayout ws_layout(const bkv_dims& d);
+
+// ---- launches (enqueue only; arguments already validated) --------------------
+hipError_t launch_ws_init(void* ws, size_t ctl_bytes, int P, int budget, hipStream_t s);
+
+hipError_t launch_beacon_update(const bkv_dims& d, const void* q_new, int T, float* beacons,
+                                int32_t* counts, int32_t* assign, hipStream_t s);
+
+hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, const void* q_win,
+                        const float* beacons, const int32_t* counts, const float* rope_cos,
+                        const float* rope_sin, float scale, float* scores, float* row_lse,
+                        void* ws, hipStream_t s);
+
+hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hipStream_t s);
+
+hipError_t launch_compact(const bkv_dims& d, const WsLayout& L, void* K, void* V,
+                          const int32_t* kept, void* ws, hipStream_t s);
+
+}  // namespace bkv

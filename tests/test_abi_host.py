@@ -1,0 +1,123 @@
+"""Host-side tests of the C ABI (no GPU needed, nothing is launched).
+
+The library must load, export every entry point include/bkv.h declares, and
+reject bad arguments on the host before anything is enqueued.  Only calls
+that fail validation are made here, with NULL pointers, so no path can reach
+a kernel launch.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+bkv = pytest.importorskip("paper_2609_04971_amd")
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "bkv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bkv_[a-z_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported():
+    names = _declared()
+    assert "bkv_evict" in names and "bkv_score" in names
+    lib = ctypes.CDLL(bkv.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in bkv.h but not exported"
+    assert sorted(bkv.EXPORTS) == names
+
+
+def test_version_and_strings():
+    assert bkv.abi_version() == 1
+    for st in range(7):
+        assert bkv.status_string(st)
+    assert bkv.status_string(0) == "ok"
+
+
+def good(**kw):
+    d = bkv.dims(B=2, Hq=8, Hkv=2, D=128, N=1000, W=8, C=4, budget=256, n_prefix=2)
+    return d.replace(**kw)
+
+
+@pytest.mark.parametrize("op", range(5))
+def test_good_dims_validate(op):
+    assert bkv.validate(good(), op) == bkv.OK
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hq=7), bkv.ERR_SHAPE),             # Hq not a multiple of Hkv
+    (dict(Hkv=0), bkv.ERR_SHAPE),
+    (dict(D=96), bkv.ERR_SHAPE),
+    (dict(N=1001, N_cap=1000), bkv.ERR_SHAPE),
+    (dict(N=-1), bkv.ERR_SHAPE),
+    (dict(budget=9), bkv.ERR_SHAPE),         # budget < W + n_prefix
+    (dict(budget=0, W=0, n_prefix=0), bkv.ERR_SHAPE),
+    (dict(C=65), bkv.ERR_SHAPE),
+    (dict(W=-1), bkv.ERR_SHAPE),
+    (dict(dtype=7), bkv.ERR_DTYPE),
+    (dict(B=-1), bkv.ERR_SHAPE),
+])
+def test_bad_dims(kw, code):
+    for op in range(5):
+        assert bkv.validate(good(**kw), op) == code
+
+
+def test_rows_needed_for_scoring_only():
+    d = good(C=0, W=0, n_prefix=0)
+    assert bkv.validate(d, bkv.OP_SCORE) == bkv.ERR_SHAPE
+    assert bkv.validate(d, bkv.OP_EVICT) == bkv.ERR_SHAPE
+    assert bkv.validate(d, bkv.OP_TOPK) == bkv.OK
+    assert bkv.validate(d, bkv.OP_COMPACT) == bkv.OK
+    assert bkv.validate(good(C=0), bkv.OP_BEACON_UPDATE) == bkv.ERR_SHAPE
+    assert bkv.validate(good(C=64, W=250), bkv.OP_SCORE) == bkv.ERR_SHAPE  # 64 + 4*250 > 1024 rows
+
+
+def test_bad_op_and_null_dims():
+    lib = bkv._lib
+    assert bkv.validate(good(), 5) == bkv.ERR_INVALID
+    assert lib.bkv_validate(None, 0) == bkv.ERR_INVALID
+    assert lib.bkv_workspace_bytes(None, 4) == 0
+
+
+def test_null_pointers_rejected_before_launch():
+    lib = bkv._lib
+    d = good()
+    r = ctypes.byref(d)
+    assert lib.bkv_score(r, None, None, None, None, None, None, 0.0, None, None, None, 0, None) == bkv.ERR_INVALID
+    assert lib.bkv_topk(r, None, None, None, 0, None) == bkv.ERR_INVALID
+    assert lib.bkv_compact(r, None, None, None, None, 0, None) == bkv.ERR_INVALID
+    assert lib.bkv_evict(r, None, None, None, None, None, None, None, 0.0, None, None, None, None, 0,
+                         None) == bkv.ERR_INVALID
+    assert lib.bkv_beacon_update(r, None, 3, None, None, None, None) == bkv.ERR_INVALID
+    assert lib.bkv_beacon_update(r, None, -1, None, None, None, None) == bkv.ERR_SHAPE
+    assert lib.bkv_workspace_init(r, None, 0, None) == bkv.ERR_INVALID
+    assert lib.bkv_device_status(None, 0, None) == bkv.ERR_INVALID
+    bad = good(D=96)
+    assert lib.bkv_evict(ctypes.byref(bad), None, None, None, None, None, None, None, 0.0, None, None, None,
+                         None, 0, None) == bkv.ERR_SHAPE
+
+
+def test_empty_work_is_a_no_op():
+    lib = bkv._lib
+    for d in (good(B=0), good(N=0)):
+        r = ctypes.byref(d)
+        assert lib.bkv_score(r, None, None, None, None, None, None, 0.0, None, None, None, 0, None) == bkv.OK
+        assert lib.bkv_topk(r, None, None, None, 0, None) == bkv.OK
+        assert lib.bkv_compact(r, None, None, None, None, 0, None) == bkv.OK
+    assert lib.bkv_beacon_update(ctypes.byref(good()), None, 0, None, None, None, None) == bkv.OK
+
+
+def test_workspace_sizes():
+    d = good()
+    assert bkv.workspace_bytes(d, bkv.OP_TOPK) == 0
+    assert bkv.workspace_bytes(d, bkv.OP_BEACON_UPDATE) == 0
+    c, s, e = (bkv.workspace_bytes(d, op) for op in (bkv.OP_COMPACT, bkv.OP_SCORE, bkv.OP_EVICT))
+    assert 0 < c < s < e
+    # the control block depends only on B*Hkv and budget, not on N, W or C
+    d2 = good(N=5000, N_cap=5000, W=16, C=8)
+    assert bkv.workspace_bytes(d2, bkv.OP_COMPACT) == c
+    assert bkv.workspace_bytes(d2, bkv.OP_EVICT) > e
+    assert bkv.workspace_bytes(good(budget=8192), bkv.OP_COMPACT) > c
