@@ -1,0 +1,197 @@
+"""Benchmark of the BeaconKV eviction step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+
+Workload: the Qwen3-4B-shaped 36-layer KV cache at 32K tokens (B=16, Hq=32,
+Hkv=8, D=128, N=32768, W=32 recent queries, C=16 beacons, budget 4096; bf16,
+77.3 GB of K/V resident in HBM), drawn on the device by
+paper_2609_04971_amd.synth.  One step is one pass of the whole hot path
+over one layer: the beacon update with that step's new queries, then the
+eviction of the layer from 32768 to 4096 tokens (score -> select ->
+compact).  Step i evicts layer i mod 36, so with the default 3 warm-up and
+30 timed steps every step meets a fresh, cache-cold 32K layer.
+
+The JSON line reports whole-step throughput (cached rows scored+compacted
+per second; a row is one (batch, kv-head, token) entry), the eviction
+latency, per-kernel times from HIP events recorded on the launch stream,
+the score kernel's roofline, and the CPU oracle timed on a sample of heads.
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+
+METRIC = "cached tokens scored+compacted/s per layer; eviction latency µs (Qwen3-4B, 32K)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--layers", type=int, default=None, help="layers resident (default: the workload's 36)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=32, help="heads in the CPU oracle sample")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported. Every (batch, kv-head) "
+              "eviction is independent, so a multi-GPU deployment shards heads with no exchange and each GPU "
+              "runs this single-GPU path on its share.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_04971_amd as bkv
+    from paper_2609_04971_amd import synth
+
+    w = synth.QWEN3_4B_32K
+    L = args.layers or w.layers
+    d = bkv.dims(B=w.B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, N=w.N, W=w.W, C=w.C, budget=w.budget, dtype=w.dtype)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    # ---- resident synthetic stack (untimed) ---------------------------------
+    t_gen = time.time()
+    layers = []
+    for l in range(L):
+        x = synth.make_layer(w, seed=l, device=dev)
+        layers.append(x)
+        if l % 6 == 5:
+            print(f"# generated {l + 1}/{L} layers", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    gen_s = time.time() - t_gen
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    scores = torch.empty(d.B, d.Hkv, d.N, device=dev)
+    kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device=dev)
+    total = args.warmup + args.steps
+    EV = ["beacon", "score", "topk", "compact"]
+    events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in EV]
+              for _ in range(total)]
+
+    def step(i):
+        x = layers[i % L]
+        ev = events[i]
+        ev[0][0].record()
+        bkv.beacon_update(d, x["q_new"], x["beacons"], x["counts"])
+        ev[0][1].record()
+        ev[1][0].record()
+        bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+                  rope_sin=x["rope_sin"])
+        ev[1][1].record()
+        ev[2][0].record()
+        bkv.topk(d, scores, kept)
+        ev[2][1].record()
+        ev[3][0].record()
+        bkv.compact(d, x["K"], x["V"], kept, ws)
+        ev[3][1].record()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, total):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    st = bkv.device_status(ws)
+    if st != bkv.OK:
+        raise SystemExit(f"device status {bkv.status_string(st)}")
+    moved = int((kept != torch.arange(d.n_keep, device=dev, dtype=torch.int32)).sum())
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    per = {k: [events[i][j][0].elapsed_time(events[i][j][1]) * 1e3 for i in range(args.warmup, total)]
+           for j, k in enumerate(EV)}
+    avg_us = {k: statistics.mean(v) for k, v in per.items()}
+    evict_us = [per["score"][i] + per["topk"][i] + per["compact"][i] for i in range(args.steps)]
+    rows = d.P * d.N
+
+    # ---- roofline of the dominant kernel (score) --------------------------
+    R = w.C + w.G * w.W
+    es = 2
+    score_bytes = rows * (w.D * es + 4)          # K read once + one fp32 score written per cached row
+    score_flops = rows * 2 * R * w.D             # logits, counted once per (row, key)
+    score_s = avg_us["score"] * 1e-6
+    achieved = score_bytes / score_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "score_kernel<bf16,128,1024-key items>",
+                "algorithmic_bytes": score_bytes,
+                "mfma_tflops": round(score_flops / score_s / 1e12, 1),
+                "mfma_frac": round(score_flops / score_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}
+    # whole eviction against HBM: K read once, scores and indices written and
+    # read back, every moved row of K and V read and written once
+    evict_bytes = rows * w.D * es + 2 * rows * 4 + 2 * d.P * d.n_keep * 4 + moved * 4 * w.D * es
+    evict_med = statistics.median(evict_us)
+
+    out = {
+        "metric": METRIC,
+        "value": round(rows / (ms_per_step * 1e-3), 1),
+        "unit": "cached rows/s per layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded generators; no model weights or datasets)",
+        "config": {"workload": f"{w.name}: per step, beacon update + evict one 32K layer to 4096 "
+                               f"(layer i mod {L} of a resident {L}-layer stack)",
+                   "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "N": w.N, "W": w.W, "C": w.C,
+                   "budget": w.budget, "layers": L},
+        "eviction_latency_us": {"median": round(evict_med, 1), "p10": round(sorted(evict_us)[len(evict_us) // 10], 1),
+                                "p90": round(sorted(evict_us)[(9 * len(evict_us)) // 10], 1)},
+        "kernel_us": {k: round(v, 2) for k, v in avg_us.items()},
+        "evict_hbm": {"algorithmic_bytes": evict_bytes, "moved_rows": moved,
+                      "achieved_GBs": round(evict_bytes / (evict_med * 1e-6) / 1e9, 1),
+                      "frac": round(evict_bytes / (evict_med * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
+        "roofline": roofline,
+        "setup_s": round(gen_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layers[0], w, args.cpu_heads)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(x, w, n_heads):
+    """The oracle's whole eviction (rows, scores, selection, compaction) on a
+    sample of heads of one freshly generated layer, on the host cores."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2609_04971_amd import synth
+
+    # regenerate layer 0's inputs (the resident copy was compacted in place)
+    g = synth.make_layer(w, seed=0, device="cuda")
+    heads = [(b, h) for b in range(w.B) for h in range(w.Hkv)][:n_heads]
+    bs = sorted({b for b, _ in heads})
+    take = lambda t: t[bs].cpu()
+    Kh, Vh, qh = take(g["K"]), take(g["V"]), take(g["q_win"])
+    bh, ch = take(g["beacons"]), take(g["counts"])
+    remap = {b: i for i, b in enumerate(bs)}
+    hl = [(remap[b], h) for b, h in heads]
+    threads = max(1, min(16, os.cpu_count() or 1))
+    t0 = time.perf_counter()
+    oracle.evict(Kh, Vh, qh, bh, ch, N=w.N, budget=w.budget, W=w.W, rope_cos=g["rope_cos"].cpu(),
+                 rope_sin=g["rope_sin"].cpu(), heads=hl, threads=threads)
+    dt = time.perf_counter() - t0
+    del g
+    return {"value": round(len(heads) * w.N / dt, 1), "unit": "cached rows/s per layer", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"{len(heads)} of {w.P} (batch, kv-head) pairs of one {w.N}-token layer, whole eviction "
+                      f"(rows, scores, selection, compaction) in double precision"}
+
+
+if __name__ == "__main__":
+    main()

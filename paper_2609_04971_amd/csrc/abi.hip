@@ -39,10 +39,7 @@ WsLayout ws_layout(const bkv_dims& d) {
     const int G = d.Hkv > 0 ? d.Hq / d.Hkv : 0;
     L.P = P;
     L.nseg = (d.budget + kSegRows - 1) / kSegRows;
-    const size_t es = d.dtype == BKV_BF16 ? 2 : 4;
     size_t off = kHdrWords * sizeof(int);
-    L.ready0 = off;
-    off = align_up(off + sizeof(int) * (size_t)P);
     L.p1cnt = off;
     off = align_up(off + sizeof(int) * (size_t)P);
     L.ready = off;
@@ -59,14 +56,10 @@ WsLayout ws_layout(const bkv_dims& d) {
     L.kgn = big >= 2048 ? 4 : 1;
     L.key_chunk = 256 * L.kgn;
     L.nch = (d.N + L.key_chunk - 1) / L.key_chunk;
-    L.Y = off;
-    off = align_up(off + es * (size_t)P * L.R_pad_max * d.D);
-    L.rowslot = off;
-    off = align_up(off + sizeof(int) * (size_t)P * L.R_pad_max);
-    L.ract = off;
-    off = align_up(off + sizeof(int) * (size_t)P);
-    L.partials = off;
-    off = align_up(off + 2 * sizeof(float) * (size_t)P * L.nch * L.R_pad_max);
+    L.part_m = off;
+    off = align_up(off + sizeof(float) * (size_t)P * L.nch * L.R_pad_max);
+    L.part_z = off;
+    off = align_up(off + sizeof(float) * (size_t)P * L.nch * L.R_pad_max);
     L.lse2 = off;
     off = align_up(off + sizeof(float) * (size_t)P * L.R_pad_max);
     L.score_end = off;

@@ -11,6 +11,11 @@
 // own first row).  Those segments hold lower tickets, have started, and
 // publish before they wait, so the waits always end.  Rows already in
 // place (kept[i] == i) are neither read nor written.
+//
+// The hazard is write-after-read only (no segment reads a row another
+// segment writes), so the hand-off needs no cache maintenance: a segment's
+// loads have returned before its flag is stored, and a writer stores only
+// after it has seen the flag.
 #include "device_common.h"
 #include "internal.h"
 
@@ -82,17 +87,17 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
             }
         });
     }
-    // Every load has returned before the flag goes up.
-    __threadfence();
+    // Every load of the workgroup has returned before the flag goes up.
+    dev::wait_all_memory();
     __syncthreads();
-    if (tid == 0) dev::st_release(a.flags + (size_t)h * a.nseg + seg, 1);
+    if (tid == 0) dev::st_flag(a.flags + (size_t)h * a.nseg + seg, 1);
     if (move) {
         // Wait for lower segments whose last source row reaches our first row.
         if (tid < 64) {
             for (int sp = tid; sp < seg; sp += 64) {
                 const int last_src = kh[min((sp + 1) * kSegRows, a.n_keep) - 1];
                 if (last_src >= i0) {
-                    if (!dev::wait_geq(a.flags + (size_t)h * a.nseg + sp, 1)) {
+                    if (!dev::wait_flag(a.flags + (size_t)h * a.nseg + sp)) {
                         s_wait_ok = 0;
                         dev::raise_error(a.hdr, kErrCompactWait);
                     }
@@ -115,14 +120,14 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
     }
     // The last item to finish clears the control block for the next launch.
     __syncthreads();
-    if (tid == 0) s_last = (dev::fetch_add_acq_rel(a.hdr + kHdrCpDone, 1) == a.total - 1);
+    if (tid == 0) s_last = (dev::fetch_add_relaxed(a.hdr + kHdrCpDone, 1) == a.total - 1);
     __syncthreads();
     if (s_last) {
         const int nf = a.P * a.nseg;
-        for (int i = tid; i < nf; i += kThreads) a.flags[i] = 0;
+        for (int i = tid; i < nf; i += kThreads) dev::st_flag(a.flags + i, 0);
         if (tid == 0) {
-            a.hdr[kHdrCpTicket] = 0;
-            a.hdr[kHdrCpDone] = 0;
+            dev::st_flag(a.hdr + kHdrCpTicket, 0);
+            dev::st_flag(a.hdr + kHdrCpDone, 0);
         }
     }
 }

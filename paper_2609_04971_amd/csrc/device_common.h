@@ -18,17 +18,25 @@ namespace dev {
 // uint4 goes through memcpy and can end up in scratch).
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Cross-workgroup hand-offs use agent-scope acquire/release: the MI355X's
-// eight XCDs have separate L2 caches, and agent scope is what makes a
-// release on one XCD visible to an acquire on another.
-__device__ inline int ld_acquire(const int* p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+// Hand-offs between work items of one launch.  The MI355X's eight XCDs
+// have separate L2 caches.  Agent-scope *atomic* loads and stores are
+// coherent across them by themselves (they carry the sc1 cache policy);
+// agent-scope acquire/release fences would instead write back and
+// invalidate whole L2 caches, which is far too slow to do per work item.
+// So data passed between work items is written and read only with these
+// atomic accesses, and ordering comes from waiting for the wave's memory
+// operations to complete before the store that publishes them.
+__device__ inline float ld_coherent(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline void st_release(int* p, int v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+__device__ inline void st_coherent(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline int fetch_add_acq_rel(int* p, int v) {
-    return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+__device__ inline int ld_flag(const int* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void st_flag(int* p, int v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ inline int fetch_add_relaxed(int* p, int v) {
     return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -36,15 +44,20 @@ __device__ inline int fetch_add_relaxed(int* p, int v) {
 __device__ inline void raise_error(int* hdr, int bits) {
     __hip_atomic_fetch_or(hdr + kHdrErr, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Wait until every load and store this wave has issued has completed
+// (s_waitcnt with all counters at zero).  Called by every thread before
+// the workgroup barrier that precedes a publishing store.
+__device__ inline void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
 
-// Bounded wait for *p >= v.  Every wait in this library is on work with a
-// lower ticket, which has already started and never waits itself, so it
-// ends; the bound only turns a broken invariant into an error instead of a
-// hang.  About 2^22 polls with a short sleep between them.
+// Bounded wait for a flag to become non-zero.  Every wait in this library
+// is on work with a lower ticket, which has already started and publishes
+// before it waits on anything, so it ends; the bound only turns a broken
+// invariant into an error instead of a hang.  About 2^22 polls with a short
+// sleep between them.
 constexpr int kSpinLimit = 1 << 22;
-__device__ inline bool wait_geq(const int* p, int v) {
+__device__ inline bool wait_flag(const int* p) {
     for (int i = 0; i < kSpinLimit; ++i) {
-        if (ld_acquire(p) >= v) return true;
+        if (ld_flag(p) != 0) return true;
         __builtin_amdgcn_s_sleep(1);
     }
     return false;

@@ -34,18 +34,15 @@ constexpr int kSegRows = 64;  // compaction rows per work item
 
 struct WsLayout {
     // control block
-    size_t ready0, p1cnt, ready;  // score: per-head flags / counters (int32 [P])
-    size_t cflags;                // compaction: per-segment read-done flags (int32 [P][nseg])
+    size_t p1cnt, ready;  // score: per-head counters / flags (int32 [P])
+    size_t cflags;        // compaction: per-segment read-done flags (int32 [P][nseg])
     size_t ctl_end;
     // data
-    size_t Y;         // assembled observation rows [P][R_pad_max][D] of the cache dtype
-    size_t rowslot;   // slot id of every row [P][R_pad_max]
-    size_t ract;      // rows per head [P]
-    size_t partials;  // per-chunk row statistics (m, z) [P][nch][R_pad_max] float2
-    size_t lse2;      // row log2-normalisers [P][R_pad_max]
+    size_t part_m, part_z;  // score: per-chunk row statistics (fp32 [P][nch][R_pad_max])
+    size_t lse2;            // score: row log2-normalisers (fp32 [P][R_pad_max])
     size_t score_end;
-    size_t scores;    // evict: scores when the caller passes none [P][N]
-    size_t kept;      // evict: kept indices when the caller passes none [P][budget]
+    size_t scores;          // evict: scores when the caller passes none [P][N]
+    size_t kept;            // evict: kept indices when the caller passes none [P][budget]
     size_t evict_end;
     int P, nseg, R_pad_max, nch, kgn, key_chunk;
 };

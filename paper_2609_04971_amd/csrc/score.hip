@@ -7,16 +7,23 @@
 // softmax attention normalised over all N keys (Eq. 4), aggregated by max
 // over every query and head of the group (Eq. 6, max form).
 //
-// One launch does it all with ticketed work items, taken in this order:
-//   A(h)     assemble head h's rows (RoPE, bf16 rounding) into the workspace;
+// One launch does it all with ticketed work items:
 //   S(h, c)  row statistics (running max m, sum z) of l over key chunk c;
 //            the last S item of a head folds them into lse_r;
 //   F(h, c)  recompute l for chunk c and write s_j = max_r (l_rj - lse_r).
 // F(h, .) is ticketed `lag` heads after S(h, .), so the second read of a
 // head's keys follows the first closely (it tends to hit the MI355X's
-// memory-side cache rather than HBM).  An item only ever waits for items
-// with lower tickets, which have already started and never wait on later
-// ones, so the schedule cannot deadlock whatever the residency.
+// memory-side cache rather than HBM).  An F item waits only for the S items
+// of its head, which hold lower tickets, have started, and never wait, so
+// the schedule cannot deadlock whatever the residency.
+//
+// Every item builds its own observation rows in LDS from the read-only
+// inputs (RoPE, then rounding to the cache dtype), so the only data passed
+// between work items are the per-chunk statistics and lse, a few KB per
+// head.  Those go through agent-scope atomic loads and stores, which are
+// coherent across the MI355X's per-XCD L2 caches by themselves; a producer
+// waits for its stores to complete (s_waitcnt) before the counter or flag
+// that publishes them, so no L2 write-back or invalidation is needed.
 //
 // Logits come from v_mfma_f32_16x16x32_bf16 (fp32 accumulation of exact
 // bf16 products; fp32 caches use v_mfma_f32_16x16x4_f32).  A lane holds a
@@ -39,6 +46,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;  // 4 waves
 constexpr int kWaves = 4;
+constexpr int kMaxC = 64;
 
 template <typename T>
 struct Tr;
@@ -65,15 +73,12 @@ struct Args {
     float* scores;
     float* row_lse;
     int* hdr;
-    int* ready0;
-    int* p1cnt;
-    int* ready;
-    void* Y;
-    int* rowslot;
-    int* ract;
-    float2* partials;
-    float* lse2;
-    int Hq, Hkv, G, N, N_cap, W, C, P, budget;
+    int* p1cnt;     // [P] S items finished per head
+    int* ready;     // [P] lse of the head published
+    float* part_m;  // [P][nch][R_pad_max] chunk row maxima (log2 units)
+    float* part_z;  // [P][nch][R_pad_max] chunk row sums relative to part_m
+    float* lse2;    // [P][R_pad_max] row log2-normalisers
+    int B, Hq, Hkv, G, N, N_cap, W, C, P, budget;
     int R_pad_max, nch, lag, total;
     float s2;     // scale * log2(e)
     float s2ln2;  // s2 * ln(2): log2-units-of-raw-dot -> natural log
@@ -157,74 +162,59 @@ __device__ __forceinline__ float2 rope_pair(float x, float y, float c, float s) 
     return make_float2(a - b, e + f);
 }
 
-// ---- A(h): assemble observation rows -------------------------------------
-template <typename T, int D>
-__device__ void assemble(const Args& a, int h, int* s_act, int* s_nact) {
-    const int tid = threadIdx.x;
-    const int b = h / a.Hkv, kh = h % a.Hkv;
-    const int32_t* cnt = a.counts + (size_t)h * a.C;  // not read when C == 0
-    if (tid == 0) {
-        int n = 0;
-        for (int c = 0; c < a.C; ++c)
-            if (cnt[c] > 0) s_act[n++] = c;
-        *s_nact = n;
-    }
-    __syncthreads();
-    const int nact = *s_nact;
-    const int R = nact + a.G * a.W;
-    const int Rp = (R + 15) & ~15;
-    T* Y = reinterpret_cast<T*>(a.Y) + (size_t)h * a.R_pad_max * D;
-    // beacon rows, rotated to the current step
-    for (int idx = tid; idx < nact * (D / 2); idx += kThreads) {
-        const int r = idx / (D / 2), i = idx % (D / 2);
-        const float* beta = a.beacons + ((size_t)h * a.C + s_act[r]) * D;
-        float2 p = make_float2(beta[i], beta[i + D / 2]);
-        if (a.rope_cos) p = rope_pair(p.x, p.y, a.rope_cos[i], a.rope_sin[i]);
-        Y[(size_t)r * D + i] = to_elem<T>(p.x);
-        Y[(size_t)r * D + i + D / 2] = to_elem<T>(p.y);
-    }
-    // recent rows: the group's G*W query rows are contiguous in q_win
-    {
-        const dev::u32x4* src = reinterpret_cast<const dev::u32x4*>(
-            reinterpret_cast<const T*>(a.qwin) + ((size_t)b * a.Hq + (size_t)kh * a.G) * a.W * D);
-        dev::u32x4* dst = reinterpret_cast<dev::u32x4*>(Y + (size_t)nact * D);
-        const int nvec = a.G * a.W * D * (int)sizeof(T) / 16;
-        for (int i = tid; i < nvec; i += kThreads) dst[i] = src[i];
-    }
-    for (int idx = tid; idx < (Rp - R) * D; idx += kThreads) Y[(size_t)R * D + idx] = T(0);
-    int* slot = a.rowslot + (size_t)h * a.R_pad_max;
-    for (int r = tid; r < Rp; r += kThreads) slot[r] = (r < nact) ? s_act[r] : (r < R ? a.C + (r - nact) : -1);
-    if (tid == 0) a.ract[h] = R;
-    if (a.row_lse) {
-        float* out = a.row_lse + (size_t)h * (a.C + a.G * a.W);
-        for (int c = tid; c < a.C; c += kThreads)
-            if (cnt[c] <= 0) out[c] = -INFINITY;
-    }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) dev::st_release(a.ready0 + h, 1);
-}
-
-// Copy rows [r0, r0 + nr) of head h's assembled rows into LDS.
-template <typename T, int D>
-__device__ __forceinline__ void rows_to_lds(const Args& a, int h, int r0, int nr, T* lds) {
-    constexpr int LD = D + Tr<T>::PAD;
-    constexpr int VPR = D * Tr<T>::ES / 16;  // 16-byte vectors per row
-    const T* Y = reinterpret_cast<const T*>(a.Y) + ((size_t)h * a.R_pad_max + r0) * D;
-    for (int i = threadIdx.x; i < nr * VPR; i += kThreads) {
-        const int r = i / VPR, v = i % VPR;
-        *reinterpret_cast<dev::u32x4*>(lds + r * LD + v * (16 / Tr<T>::ES)) =
-            reinterpret_cast<const dev::u32x4*>(Y + (size_t)r * D)[v];
-    }
-}
-
 template <typename T, int D>
 struct alignas(16) Smem {
     T y[Tr<T>::RG * (D + Tr<T>::PAD)];
     float red_m[kWaves][Tr<T>::RG];
     float red_z[kWaves][Tr<T>::RG];
     float nlse[Tr<T>::RG];
+    int act[kMaxC];
+    int nact;
 };
+
+// Occupied beacon slots of head h, ascending, into sm.act / sm.nact.
+template <typename T, int D>
+__device__ __forceinline__ void active_slots(const Args& a, int h, Smem<T, D>& sm) {
+    if (threadIdx.x == 0) {
+        const int32_t* cnt = a.counts + (size_t)h * a.C;  // not read when C == 0
+        int n = 0;
+        for (int c = 0; c < a.C; ++c)
+            if (cnt[c] > 0) sm.act[n++] = c;
+        sm.nact = n;
+    }
+    __syncthreads();
+}
+
+// Observation rows [r0, r0 + nr) of head h into LDS: rows below nact are
+// the occupied beacons rotated to the step and rounded to the cache dtype,
+// then the G*W recent queries (contiguous in q_win), then zero padding.
+template <typename T, int D>
+__device__ void build_rows(const Args& a, int h, int r0, int nr, Smem<T, D>& sm) {
+    constexpr int LD = D + Tr<T>::PAD;
+    constexpr int VPR = D * Tr<T>::ES / 16;
+    const int tid = threadIdx.x;
+    const int b = h / a.Hkv, kh = h % a.Hkv;
+    const int nact = sm.nact, R = nact + a.G * a.W;
+    // beacon rows in this group
+    const int bl = max(0, min(nact, r0 + nr) - r0);
+    for (int idx = tid; idx < bl * (D / 2); idx += kThreads) {
+        const int r = idx / (D / 2), i = idx % (D / 2);
+        const float* beta = a.beacons + ((size_t)h * a.C + sm.act[r0 + r]) * D;
+        float2 p = make_float2(beta[i], beta[i + D / 2]);
+        if (a.rope_cos) p = rope_pair(p.x, p.y, a.rope_cos[i], a.rope_sin[i]);
+        sm.y[r * LD + i] = to_elem<T>(p.x);
+        sm.y[r * LD + i + D / 2] = to_elem<T>(p.y);
+    }
+    // recent rows and padding, 16 bytes at a time
+    const T* q = reinterpret_cast<const T*>(a.qwin) + ((size_t)b * a.Hq + (size_t)kh * a.G) * a.W * D;
+    for (int i = tid; i < (nr - bl) * VPR; i += kThreads) {
+        const int r = bl + i / VPR, v = i % VPR;
+        const int gr = r0 + r;  // row index within the head
+        dev::u32x4 val = {0u, 0u, 0u, 0u};
+        if (gr < R) val = reinterpret_cast<const dev::u32x4*>(q + (size_t)(gr - nact) * D)[v];
+        *reinterpret_cast<dev::u32x4*>(sm.y + r * LD + v * (16 / Tr<T>::ES)) = val;
+    }
+}
 
 // ---- S(h, chunk): row statistics over one key chunk -------------------------
 template <typename T, int D, int KGN>
@@ -233,18 +223,20 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     constexpr int KC = kWaves * 64 * KGN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int R = a.ract[h];
+    active_slots<T, D>(a, h, sm);
+    const int nact = sm.nact;
+    const int R = nact + a.G * a.W;
     const int Rp = (R + 15) & ~15;
     const T* Kh = reinterpret_cast<const T*>(a.K) + (size_t)h * a.N_cap * D;
     const int kw = chunk * KC + wave * 64 * KGN;  // this wave's first key
     const int N = a.N;
     const float s2 = a.s2;
-    float2* part = a.partials + ((size_t)h * a.nch + chunk) * a.R_pad_max;
+    const size_t pbase = ((size_t)h * a.nch + chunk) * a.R_pad_max;
 
     for (int r0 = 0; r0 < Rp; r0 += RG) {
         const int nr = min(RG, Rp - r0), RT = nr / 16;
         __syncthreads();
-        rows_to_lds<T, D>(a, h, r0, nr, sm.y);
+        build_rows<T, D>(a, h, r0, nr, sm);
         __syncthreads();
         float m[RTM], z[RTM];
 #pragma unroll
@@ -309,32 +301,40 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             float mm = sm.red_m[0][r], zz = sm.red_z[0][r];
 #pragma unroll
             for (int w = 1; w < kWaves; ++w) merge_mz(mm, zz, sm.red_m[w][r], sm.red_z[w][r]);
-            part[r0 + r] = make_float2(mm, zz);
+            dev::st_coherent(a.part_m + pbase + r0 + r, mm);
+            dev::st_coherent(a.part_z + pbase + r0 + r, zz);
         }
     }
-    // publish; the last chunk of the head folds the statistics into lse
-    __threadfence();
+    // publish: statistics stored before the counter moves
+    dev::wait_all_memory();
     __syncthreads();
-    if (tid == 0) *s_flag = (dev::fetch_add_acq_rel(a.p1cnt + h, 1) == a.nch - 1);
+    if (tid == 0) *s_flag = (dev::fetch_add_relaxed(a.p1cnt + h, 1) == a.nch - 1);
     __syncthreads();
     if (!*s_flag) return;
-    const float2* ph = a.partials + (size_t)h * a.nch * a.R_pad_max;
-    const int* slot = a.rowslot + (size_t)h * a.R_pad_max;
-    float* lse2 = a.lse2 + (size_t)h * a.R_pad_max;
+    // last chunk of the head: fold the chunk statistics into lse
+    const size_t hb = (size_t)h * a.nch * a.R_pad_max;
     for (int r = tid; r < Rp; r += kThreads) {
         float mm = -INFINITY, zz = 0.f;
         if (r < R)
             for (int c = 0; c < a.nch; ++c) {
-                const float2 p = ph[(size_t)c * a.R_pad_max + r];
-                merge_mz(mm, zz, p.x, p.y);
+                const size_t i = hb + (size_t)c * a.R_pad_max + r;
+                merge_mz(mm, zz, dev::ld_coherent(a.part_m + i), dev::ld_coherent(a.part_z + i));
             }
         const float l2 = (r < R) ? mm + log2f(zz) : INFINITY;  // padding rows never win
-        lse2[r] = l2;
-        if (a.row_lse && r < R) a.row_lse[(size_t)h * (a.C + a.G * a.W) + slot[r]] = l2 * 0.69314718055994531f;
+        dev::st_coherent(a.lse2 + (size_t)h * a.R_pad_max + r, l2);
+        if (a.row_lse && r < R) {
+            const int slot = (r < nact) ? sm.act[r] : a.C + (r - nact);
+            a.row_lse[(size_t)h * (a.C + a.G * a.W) + slot] = l2 * 0.69314718055994531f;
+        }
     }
-    __threadfence();
+    if (a.row_lse) {  // empty beacon slots have no row
+        const int32_t* cnt = a.counts + (size_t)h * a.C;
+        for (int c = tid; c < a.C; c += kThreads)
+            if (cnt[c] <= 0) a.row_lse[(size_t)h * (a.C + a.G * a.W) + c] = -INFINITY;
+    }
+    dev::wait_all_memory();
     __syncthreads();
-    if (tid == 0) dev::st_release(a.ready + h, 1);
+    if (tid == 0) dev::st_flag(a.ready + h, 1);
 }
 
 // ---- F(h, chunk): final max-aggregated scores over one key chunk ----------
@@ -344,13 +344,13 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm) {
     constexpr int KC = kWaves * 64 * KGN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int R = a.ract[h];
+    active_slots<T, D>(a, h, sm);
+    const int R = sm.nact + a.G * a.W;
     const int Rp = (R + 15) & ~15;
     const T* Kh = reinterpret_cast<const T*>(a.K) + (size_t)h * a.N_cap * D;
     const int kw = chunk * KC + wave * 64 * KGN;
     const int N = a.N;
     const float inv_s2 = 1.0f / a.s2;
-    const float* lse2 = a.lse2 + (size_t)h * a.R_pad_max;
 
     float best[4 * KGN];
 #pragma unroll
@@ -359,8 +359,9 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm) {
     for (int r0 = 0; r0 < Rp; r0 += RG) {
         const int nr = min(RG, Rp - r0), RT = nr / 16;
         __syncthreads();
-        rows_to_lds<T, D>(a, h, r0, nr, sm.y);
-        for (int r = tid; r < nr; r += kThreads) sm.nlse[r] = -lse2[r0 + r] * inv_s2;
+        build_rows<T, D>(a, h, r0, nr, sm);
+        for (int r = tid; r < nr; r += kThreads)
+            sm.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r0 + r) * inv_s2;
         __syncthreads();
 #pragma unroll
         for (int kg = 0; kg < KGN; ++kg) {
@@ -398,16 +399,10 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm) {
     }
 }
 
-// Ticket -> work item.  kind 0 = A, 1 = S, 2 = F.
+// Ticket -> work item.  kind 1 = S, 2 = F.  The S items of head h come
+// `lag` heads before its F items.
 __device__ __forceinline__ void decode(const Args& a, int t, int& kind, int& h, int& c) {
     const int P = a.P, nch = a.nch, L = a.lag;
-    if (t < P) {
-        kind = 0;
-        h = t;
-        c = 0;
-        return;
-    }
-    t -= P;
     if (t < L * nch) {
         kind = 1;
         h = t / nch;
@@ -437,8 +432,7 @@ __device__ __forceinline__ void decode(const Args& a, int t, int& kind, int& h, 
 template <typename T, int D, int KGN>
 __global__ __launch_bounds__(kThreads) void score_kernel(Args a) {
     __shared__ Smem<T, D> sm;
-    __shared__ int s_ticket, s_ok, s_flag, s_nact;
-    __shared__ int s_act[64];
+    __shared__ int s_ticket, s_ok, s_flag;
     const int tid = threadIdx.x;
     if (tid == 0) {
         s_ok = dev::stamp_ok(a.hdr, a.P, a.budget);
@@ -455,35 +449,28 @@ __global__ __launch_bounds__(kThreads) void score_kernel(Args a) {
     }
     int kind, h, c;
     decode(a, s_ticket, kind, h, c);
-    if (kind == 0) {
-        assemble<T, D>(a, h, s_act, &s_nact);
+    if (kind == 1) {
+        stats_item<T, D, KGN>(a, h, c, sm, &s_flag);
     } else {
-        int* flag = (kind == 1) ? a.ready0 + h : a.ready + h;
         if (tid == 0) {
-            s_flag = dev::wait_geq(flag, 1);
+            s_flag = dev::wait_flag(a.ready + h);
             if (!s_flag) dev::raise_error(a.hdr, kErrScoreWait);
         }
         __syncthreads();
-        if (s_flag) {
-            if (kind == 1)
-                stats_item<T, D, KGN>(a, h, c, sm, &s_flag);
-            else
-                final_item<T, D, KGN>(a, h, c, sm);
-        }
+        if (s_flag) final_item<T, D, KGN>(a, h, c, sm);
     }
     // The last item to finish clears the control block for the next launch.
     __syncthreads();
-    if (tid == 0) s_flag = (dev::fetch_add_acq_rel(a.hdr + kHdrScDone, 1) == a.total - 1);
+    if (tid == 0) s_flag = (dev::fetch_add_relaxed(a.hdr + kHdrScDone, 1) == a.total - 1);
     __syncthreads();
     if (s_flag) {
         for (int i = tid; i < a.P; i += kThreads) {
-            a.ready0[i] = 0;
-            a.p1cnt[i] = 0;
-            a.ready[i] = 0;
+            dev::st_flag(a.p1cnt + i, 0);
+            dev::st_flag(a.ready + i, 0);
         }
         if (tid == 0) {
-            a.hdr[kHdrScTicket] = 0;
-            a.hdr[kHdrScDone] = 0;
+            dev::st_flag(a.hdr + kHdrScTicket, 0);
+            dev::st_flag(a.hdr + kHdrScDone, 0);
         }
     }
 }
@@ -511,14 +498,12 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
     a.scores = scores;
     a.row_lse = row_lse;
     a.hdr = reinterpret_cast<int*>(w);
-    a.ready0 = reinterpret_cast<int*>(w + L.ready0);
     a.p1cnt = reinterpret_cast<int*>(w + L.p1cnt);
     a.ready = reinterpret_cast<int*>(w + L.ready);
-    a.Y = w + L.Y;
-    a.rowslot = reinterpret_cast<int*>(w + L.rowslot);
-    a.ract = reinterpret_cast<int*>(w + L.ract);
-    a.partials = reinterpret_cast<float2*>(w + L.partials);
+    a.part_m = reinterpret_cast<float*>(w + L.part_m);
+    a.part_z = reinterpret_cast<float*>(w + L.part_z);
     a.lse2 = reinterpret_cast<float*>(w + L.lse2);
+    a.B = d.B;
     a.Hq = d.Hq;
     a.Hkv = d.Hkv;
     a.G = d.Hq / d.Hkv;
@@ -537,7 +522,7 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
         cus = 256;
     int lag = (2 * cus + 2 * L.nch - 1) / (2 * L.nch);
     a.lag = lag < 1 ? 1 : (lag > L.P ? L.P : lag);
-    a.total = L.P + 2 * L.P * L.nch;
+    a.total = 2 * L.P * L.nch;
     const float sc = (scale == 0.0f) ? (float)(1.0 / sqrt((double)d.D)) : scale;
     a.s2 = sc * 1.4426950408889634f;
     a.s2ln2 = a.s2 * 0.69314718055994531f;

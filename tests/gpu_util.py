@@ -52,7 +52,8 @@ def assert_scores_close(got: np.ndarray, want: np.ndarray, what="scores"):
     want = np.asarray(want, np.float64)
     both_inf = np.isneginf(got) & np.isneginf(want)
     assert not np.isnan(got).any(), f"{what}: NaN in GPU output"
-    err = np.where(both_inf, 0.0, np.abs(got - want))
+    with np.errstate(invalid="ignore"):
+        err = np.where(both_inf, 0.0, np.abs(got - want))
     worst = np.unravel_index(np.argmax(err), err.shape)
     assert err.max() <= SCORE_TOL, f"{what}: max |diff| {err.max():.3g} at {worst} (gpu {got[worst]}, ref {want[worst]})"
     return float(err.max())
