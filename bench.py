@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="layers resident (default: the workload's 36)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=32, help="heads in the CPU oracle sample")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
+                         "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
     return ap.parse_args()
 
 
@@ -63,6 +66,13 @@ def main():
     d = bkv.dims(B=w.B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, N=w.N, W=w.W, C=w.C, budget=w.budget, dtype=w.dtype)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.calibrate:
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- resident synthetic stack (untimed) ---------------------------------
     t_gen = time.time()

@@ -4,8 +4,8 @@ Argument marshalling only: every step of the path runs in the HIP kernels
 behind include/bkv.h.  torch supplies device memory and the stream (work is
 enqueued on torch's current stream).  Tensor shapes, dtypes, devices and
 contiguity are checked here because the C ABI takes bare pointers and
-cannot see them.  There is no fallback: if the library is not built this
-module fails to import.
+cannot see them.  There is no fallback: the library is loaded on first use,
+and if it is not built that first use raises ImportError.
 """
 from __future__ import annotations
 
@@ -16,11 +16,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libbkv.so")
-
-if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_04971_amd.build`")
-
-_lib = ctypes.CDLL(LIB_PATH)
+_lib = None
 
 OK, ERR_INVALID, ERR_SHAPE, ERR_DTYPE, ERR_WORKSPACE, ERR_HIP, ERR_DEVICE = range(7)
 F32, BF16 = 0, 1
@@ -69,28 +65,34 @@ def dims(B, Hq, Hkv, D, N, W, C, budget, n_prefix=0, dtype="bf16", N_cap=None) -
 _P = ctypes.c_void_p
 _D = ctypes.POINTER(Dims)
 _S = ctypes.c_size_t
-_lib.bkv_validate.argtypes = [_D, ctypes.c_int32]
-_lib.bkv_validate.restype = ctypes.c_int
-_lib.bkv_workspace_bytes.argtypes = [_D, ctypes.c_int32]
-_lib.bkv_workspace_bytes.restype = _S
-_lib.bkv_workspace_init.argtypes = [_D, _P, _S, _P]
-_lib.bkv_workspace_init.restype = ctypes.c_int
-_lib.bkv_device_status.argtypes = [_P, _S, _P]
-_lib.bkv_device_status.restype = ctypes.c_int
-_lib.bkv_beacon_update.argtypes = [_D, _P, ctypes.c_int32, _P, _P, _P, _P]
-_lib.bkv_beacon_update.restype = ctypes.c_int
-_lib.bkv_score.argtypes = [_D, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _S, _P]
-_lib.bkv_score.restype = ctypes.c_int
-_lib.bkv_topk.argtypes = [_D, _P, _P, _P, _S, _P]
-_lib.bkv_topk.restype = ctypes.c_int
-_lib.bkv_compact.argtypes = [_D, _P, _P, _P, _P, _S, _P]
-_lib.bkv_compact.restype = ctypes.c_int
-_lib.bkv_evict.argtypes = [_D, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P]
-_lib.bkv_evict.restype = ctypes.c_int
-_lib.bkv_status_string.argtypes = [ctypes.c_int]
-_lib.bkv_status_string.restype = ctypes.c_char_p
-_lib.bkv_abi_version.argtypes = []
-_lib.bkv_abi_version.restype = ctypes.c_int32
+_SIGS = {
+    "bkv_validate": ([_D, ctypes.c_int32], ctypes.c_int),
+    "bkv_workspace_bytes": ([_D, ctypes.c_int32], _S),
+    "bkv_workspace_init": ([_D, _P, _S, _P], ctypes.c_int),
+    "bkv_device_status": ([_P, _S, _P], ctypes.c_int),
+    "bkv_beacon_update": ([_D, _P, ctypes.c_int32, _P, _P, _P, _P], ctypes.c_int),
+    "bkv_score": ([_D, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_topk": ([_D, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_compact": ([_D, _P, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_evict": ([_D, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "bkv_abi_version": ([], ctypes.c_int32),
+}
+
+
+def lib():
+    """The loaded libbkv.so (loaded on first use; ImportError if not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_04971_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
 
 
 class BkvError(RuntimeError):
@@ -100,11 +102,11 @@ class BkvError(RuntimeError):
 
 
 def status_string(st: int) -> str:
-    return _lib.bkv_status_string(st).decode()
+    return lib().bkv_status_string(st).decode()
 
 
 def abi_version() -> int:
-    return int(_lib.bkv_abi_version())
+    return int(lib().bkv_abi_version())
 
 
 def _check(st: int, where: str):
@@ -114,11 +116,11 @@ def _check(st: int, where: str):
 
 def validate(d: Dims, op: int) -> int:
     """Host-only validation (no GPU needed); returns the bkv_status code."""
-    return int(_lib.bkv_validate(ctypes.byref(d), op))
+    return int(lib().bkv_validate(ctypes.byref(d), op))
 
 
 def workspace_bytes(d: Dims, op: int = OP_EVICT) -> int:
-    return int(_lib.bkv_workspace_bytes(ctypes.byref(d), op))
+    return int(lib().bkv_workspace_bytes(ctypes.byref(d), op))
 
 
 # ---- marshalling helpers ---------------------------------------------------
@@ -165,20 +167,20 @@ def workspace(d: Dims, op: int = OP_EVICT, device="cuda") -> torch.Tensor:
 
 def workspace_init(d: Dims, ws: torch.Tensor):
     p, n = _ws(ws)
-    _check(_lib.bkv_workspace_init(ctypes.byref(d), p, n, _stream()), "bkv_workspace_init")
+    _check(lib().bkv_workspace_init(ctypes.byref(d), p, n, _stream()), "bkv_workspace_init")
 
 
 def device_status(ws: torch.Tensor) -> int:
     """Synchronise the current stream and return the workspace's device status."""
     p, n = _ws(ws)
-    return int(_lib.bkv_device_status(p, n, _stream()))
+    return int(lib().bkv_device_status(p, n, _stream()))
 
 
 # ---- operations ------------------------------------------------------------------
 def beacon_update(d: Dims, q_new, beacons, counts, assign=None):
     """(a1) in place on beacons [B,Hkv,C,D] fp32 and counts [B,Hkv,C] int32."""
     T = q_new.shape[2]
-    st = _lib.bkv_beacon_update(
+    st = lib().bkv_beacon_update(
         ctypes.byref(d), _ptr(q_new, (d.B, d.Hq, T, d.D), _tdtype(d), "q_new"), T,
         _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
         _ptr(counts, (d.B, d.Hkv, d.C), torch.int32, "counts"),
@@ -196,7 +198,7 @@ def score(d: Dims, K, q_win, beacons, counts, scores, ws, row_lse=None, rope_cos
     """(a2)+(a3): scores [B,Hkv,N] fp32 (and row_lse [B,Hkv,C+G*W]) written."""
     rc, rs = _rope(rope_cos, rope_sin, d)
     wp, wn = _ws(ws)
-    st = _lib.bkv_score(
+    st = lib().bkv_score(
         ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
         _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),
         _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
@@ -210,7 +212,7 @@ def score(d: Dims, K, q_win, beacons, counts, scores, ws, row_lse=None, rope_cos
 def topk(d: Dims, scores, kept, ws=None):
     """(a4): kept [B,Hkv,min(budget,N)] int32 written, ascending."""
     wp, wn = _ws(ws)
-    st = _lib.bkv_topk(ctypes.byref(d), _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores"),
+    st = lib().bkv_topk(ctypes.byref(d), _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores"),
                        _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept"), wp, wn, _stream())
     _check(st, "bkv_topk")
 
@@ -218,7 +220,7 @@ def topk(d: Dims, scores, kept, ws=None):
 def compact(d: Dims, K, V, kept, ws):
     """(a5): rows i < n of K and V become rows kept[i], in place."""
     wp, wn = _ws(ws)
-    st = _lib.bkv_compact(ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+    st = lib().bkv_compact(ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
                           _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
                           _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept"), wp, wn, _stream())
     _check(st, "bkv_compact")
@@ -229,7 +231,7 @@ def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row
     """(a6): score -> select -> compact one layer in place."""
     rc, rs = _rope(rope_cos, rope_sin, d)
     wp, wn = _ws(ws)
-    st = _lib.bkv_evict(
+    st = lib().bkv_evict(
         ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
         _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
         _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),

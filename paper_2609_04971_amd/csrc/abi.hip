@@ -40,10 +40,8 @@ WsLayout ws_layout(const bkv_dims& d) {
     L.P = P;
     L.nseg = (d.budget + kSegRows - 1) / kSegRows;
     size_t off = kHdrWords * sizeof(int);
-    L.p1cnt = off;
-    off = align_up(off + sizeof(int) * (size_t)P);
-    L.ready = off;
-    off = align_up(off + sizeof(int) * (size_t)P);
+    L.hctl = off;
+    off = align_up(off + sizeof(int) * (size_t)P * kHcWords);
     L.cflags = off;
     off = align_up(off + sizeof(int) * (size_t)P * L.nseg);
     L.ctl_end = off;

@@ -3,8 +3,9 @@
 // after Sort).  HBM-bound: every moved row is read once and written once.
 //
 // kept is strictly ascending, so kept[i] >= i: a row only ever moves
-// towards the front.  Work items are segments of kSegRows destination rows,
-// ticketed head-major.  A segment first loads all of its source rows into
+// towards the front.  Work items are segments of kSegRows destination rows;
+// each head's workgroups take their segment numbers from a per-head ticket,
+// so segments of a head start in order.  A segment first loads all of its source rows into
 // registers and publishes "read done"; before writing it waits for every
 // lower segment of the same head whose sources reach into its destination
 // rows (only lower segments can: a segment's sources lie at or after its
@@ -29,6 +30,7 @@ struct Args {
     char* V;
     const int32_t* kept;
     int* hdr;
+    int* hctl;   // [P][kHcWords] per-head control lines
     int* flags;  // [P][nseg] read-done flags
     int P, budget, N, n_keep, nseg, total;
     size_t head_stride;  // bytes between heads (N_cap * row bytes)
@@ -42,10 +44,12 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
     __shared__ int s_ticket, s_ok, s_move, s_bad, s_wait_ok, s_last;
     __shared__ int s_src[kSegRows];
     const int tid = threadIdx.x;
+    const int h = blockIdx.x / a.nseg;
+    int* hc = a.hctl + (size_t)h * kHcWords;
     if (tid == 0) {
         s_ok = dev::stamp_ok(a.hdr, a.P, a.budget);
         if (s_ok)
-            s_ticket = dev::fetch_add_relaxed(a.hdr + kHdrCpTicket, 1);
+            s_ticket = dev::fetch_add_relaxed(hc + kHcCpTicket, 1);
         else
             dev::raise_error(a.hdr, kErrStamp);
         s_move = 0;
@@ -54,11 +58,11 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
     }
     __syncthreads();
     if (!s_ok) return;
-    if (s_ticket >= a.total) {  // control block was not clear: do nothing
+    if (s_ticket >= a.nseg) {  // control block was not clear: do nothing
         if (tid == 0) dev::raise_error(a.hdr, kErrStamp);
         return;
     }
-    const int h = s_ticket / a.nseg, seg = s_ticket % a.nseg;
+    const int seg = s_ticket;  // segments of a head start in ticket order
     const int i0 = seg * kSegRows;
     const int rows = min(kSegRows, a.n_keep - i0);
     const int32_t* kh = a.kept + (size_t)h * a.n_keep;
@@ -120,14 +124,13 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
     }
     // The last item to finish clears the control block for the next launch.
     __syncthreads();
-    if (tid == 0) s_last = (dev::fetch_add_relaxed(a.hdr + kHdrCpDone, 1) == a.total - 1);
+    if (tid == 0) s_last = (dev::fetch_add_relaxed(hc + kHcCpDone, 1) == a.nseg - 1);
     __syncthreads();
-    if (s_last) {
-        const int nf = a.P * a.nseg;
-        for (int i = tid; i < nf; i += kThreads) dev::st_flag(a.flags + i, 0);
+    if (s_last) {  // every segment of the head is done: clear its control words
+        for (int i = tid; i < a.nseg; i += kThreads) dev::st_flag(a.flags + (size_t)h * a.nseg + i, 0);
         if (tid == 0) {
-            dev::st_flag(a.hdr + kHdrCpTicket, 0);
-            dev::st_flag(a.hdr + kHdrCpDone, 0);
+            dev::st_flag(hc + kHcCpTicket, 0);
+            dev::st_flag(hc + kHcCpDone, 0);
         }
     }
 }
@@ -142,6 +145,7 @@ hipError_t launch_compact(const bkv_dims& d, const WsLayout& L, void* K, void* V
     a.V = static_cast<char*>(V);
     a.kept = kept;
     a.hdr = reinterpret_cast<int*>(w);
+    a.hctl = reinterpret_cast<int*>(w + L.hctl);
     a.flags = reinterpret_cast<int*>(w + L.cflags);
     a.P = L.P;
     a.budget = d.budget;

@@ -20,12 +20,20 @@ enum HdrWord : int {
     kHdrMagic = 0,
     kHdrP = 1,
     kHdrBudget = 2,
-    kHdrErr = 3,        // sticky device error bits, cleared only by init
-    kHdrScTicket = 4,   // score kernel work ticket
-    kHdrScDone = 5,     // score kernel finished work items
-    kHdrCpTicket = 6,   // compaction kernel work ticket
-    kHdrCpDone = 7,     // compaction kernel finished work items
-    kHdrWords = 64      // header is 256 bytes
+    kHdrErr = 3,     // sticky device error bits, cleared only by init
+    kHdrWords = 64   // header is 256 bytes
+};
+
+// One 128-byte control line per (batch, kv-head), so that work items of
+// different heads never contend for one address.
+enum HeadWord : int {
+    kHcScTicket = 0,  // score: work ticket within the head
+    kHcScDone = 1,    // score: work items of the head finished
+    kHcP1Count = 2,   // score: statistics items of the head finished
+    kHcReady = 3,     // score: the head's row normalisers are published
+    kHcCpTicket = 4,  // compaction: work ticket within the head
+    kHcCpDone = 5,    // compaction: segments of the head finished
+    kHcWords = 32
 };
 
 enum DevErr : int { kErrScoreWait = 1, kErrCompactWait = 2, kErrStamp = 4, kErrBadIndex = 8 };
@@ -34,8 +42,8 @@ constexpr int kSegRows = 64;  // compaction rows per work item
 
 struct WsLayout {
     // control block
-    size_t p1cnt, ready;  // score: per-head counters / flags (int32 [P])
-    size_t cflags;        // compaction: per-segment read-done flags (int32 [P][nseg])
+    size_t hctl;    // per-head control lines (int32 [P][kHcWords])
+    size_t cflags;  // compaction: per-segment read-done flags (int32 [P][nseg])
     size_t ctl_end;
     // data
     size_t part_m, part_z;  // score: per-chunk row statistics (fp32 [P][nch][R_pad_max])

@@ -7,15 +7,18 @@
 // softmax attention normalised over all N keys (Eq. 4), aggregated by max
 // over every query and head of the group (Eq. 6, max form).
 //
-// One launch does it all with ticketed work items:
+// One launch does it all.  Each head gets 2 * nch workgroups, which take a
+// per-head ticket when they start: the first nch tickets are
 //   S(h, c)  row statistics (running max m, sum z) of l over key chunk c;
 //            the last S item of a head folds them into lse_r;
+// and the next nch are
 //   F(h, c)  recompute l for chunk c and write s_j = max_r (l_rj - lse_r).
-// F(h, .) is ticketed `lag` heads after S(h, .), so the second read of a
-// head's keys follows the first closely (it tends to hit the MI355X's
-// memory-side cache rather than HBM).  An F item waits only for the S items
-// of its head, which hold lower tickets, have started, and never wait, so
-// the schedule cannot deadlock whatever the residency.
+// An F item waits only for the S items of its head, which hold lower
+// tickets, have started, and never wait, so the schedule cannot deadlock
+// whatever the residency.  The grid lists a head's workgroups `lag` heads
+// after the head's first ones, so the second read of a head's keys follows
+// the first closely (it tends to hit the MI355X's memory-side cache rather
+// than HBM).
 //
 // Every item builds its own observation rows in LDS from the read-only
 // inputs (RoPE, then rounding to the cache dtype), so the only data passed
@@ -26,10 +29,10 @@
 // that publishes them, so no L2 write-back or invalidation is needed.
 //
 // Logits come from v_mfma_f32_16x16x32_bf16 (fp32 accumulation of exact
-// bf16 products; fp32 caches use v_mfma_f32_16x16x4_f32).  A lane holds a
-// contiguous quarter of a row (D/4 elements) of each 16-row operand tile,
-// so the key tile is read straight from HBM with 16-byte loads, no LDS
-// staging; the observation rows sit in LDS.  Statistics are kept in log2
+// bf16 products; fp32 caches use v_mfma_f32_16x16x4_f32).  Key tiles are
+// read straight from HBM into MFMA operand registers with 16-byte loads (no
+// LDS staging), laid out so each load instruction covers 64 contiguous
+// bytes of each of 16 rows; the observation rows sit in LDS.  Statistics are kept in log2
 // units (v_exp_f32 computes 2^x): s2 = scale * log2(e).  In F items the
 // accumulator starts at -lse2_r / s2, so the MFMA yields l_rj - lse_r (up
 // to the factor s2) directly and the epilogue is one max per element.
@@ -54,13 +57,13 @@ template <>
 struct Tr<uint16_t> {  // bf16 storage
     static constexpr int ES = 2;
     static constexpr int PAD = 8;   // LDS row padding, elements (16 bytes)
-    static constexpr int RG = 160;  // observation rows resident in LDS at a time
+    static constexpr int RG = 144;  // observation rows resident in LDS at a time
 };
 template <>
 struct Tr<float> {
     static constexpr int ES = 4;
     static constexpr int PAD = 4;
-    static constexpr int RG = 80;
+    static constexpr int RG = 64;
 };
 
 struct Args {
@@ -73,8 +76,7 @@ struct Args {
     float* scores;
     float* row_lse;
     int* hdr;
-    int* p1cnt;     // [P] S items finished per head
-    int* ready;     // [P] lse of the head published
+    int* hctl;      // [P][kHcWords] per-head control lines
     float* part_m;  // [P][nch][R_pad_max] chunk row maxima (log2 units)
     float* part_z;  // [P][nch][R_pad_max] chunk row sums relative to part_m
     float* lse2;    // [P][R_pad_max] row log2-normalisers
@@ -84,26 +86,32 @@ struct Args {
     float s2ln2;  // s2 * ln(2): log2-units-of-raw-dot -> natural log
 };
 
-// Per-lane operand slice: D/4 contiguous elements = NV 16-byte vectors.
+// Per-lane operand: NV 16-byte vectors of one row.  Vector v of lane group
+// g (lane >> 4) holds bytes [64 v + 16 g, 64 v + 16 g + 16) of the row, so
+// the four lane groups of a load instruction read 64 contiguous bytes of
+// each row and two consecutive instructions complete a 128-byte line.  For
+// bf16 vector v is one MFMA step (k = 32 elements); for fp32 it is four.
 template <typename T, int D>
 struct Op {
-    static constexpr int SL = D / 4;
-    static constexpr int NV = SL * Tr<T>::ES / 16;
+    static constexpr int NV = D * Tr<T>::ES / 64;
+    static constexpr int EV = 16 / Tr<T>::ES;  // elements per vector
     dev::u32x4 v[NV];
 };
 
 template <typename T, int D>
 __device__ __forceinline__ void load_key_tile(Op<T, D>& op, const T* Khead, int key, int g) {
-    const dev::u32x4* src = reinterpret_cast<const dev::u32x4*>(Khead + (size_t)key * D + g * Op<T, D>::SL);
+    const T* row = Khead + (size_t)key * D + g * Op<T, D>::EV;
 #pragma unroll
-    for (int v = 0; v < Op<T, D>::NV; ++v) op.v[v] = src[v];
+    for (int v = 0; v < Op<T, D>::NV; ++v)
+        op.v[v] = *reinterpret_cast<const dev::u32x4*>(row + v * 4 * Op<T, D>::EV);
 }
 
 template <typename T, int D>
-__device__ __forceinline__ void load_row_tile(Op<T, D>& op, const T* lds_row) {
-    const dev::u32x4* src = reinterpret_cast<const dev::u32x4*>(lds_row);
+__device__ __forceinline__ void load_row_tile(Op<T, D>& op, const T* lds_row, int g) {
+    const T* row = lds_row + g * Op<T, D>::EV;
 #pragma unroll
-    for (int v = 0; v < Op<T, D>::NV; ++v) op.v[v] = src[v];
+    for (int v = 0; v < Op<T, D>::NV; ++v)
+        op.v[v] = *reinterpret_cast<const dev::u32x4*>(row + v * 4 * Op<T, D>::EV);
 }
 
 // acc += A * B over the whole head dimension; A supplies the output rows
@@ -162,48 +170,55 @@ __device__ __forceinline__ float2 rope_pair(float x, float y, float c, float s) 
     return make_float2(a - b, e + f);
 }
 
+// The four 16-key tiles of one 64-key group (keys past N read key N-1).
+template <typename T, int D>
+__device__ __forceinline__ void load_group(Op<T, D>* kop, const T* Kh, int kb, int N, int c16, int g) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) load_key_tile<T, D>(kop[t], Kh, min(kb + t * 16 + c16, N - 1), g);
+}
+
 template <typename T, int D>
 struct alignas(16) Smem {
     T y[Tr<T>::RG * (D + Tr<T>::PAD)];
     float red_m[kWaves][Tr<T>::RG];
     float red_z[kWaves][Tr<T>::RG];
     float nlse[Tr<T>::RG];
+    float best[kWaves * 64 * 4];  // F items: per-key maxima of the chunk (up to 1024 keys)
     int act[kMaxC];
     int nact;
 };
 
-// Occupied beacon slots of head h, ascending, into sm.act / sm.nact.
-template <typename T, int D>
-__device__ __forceinline__ void active_slots(const Args& a, int h, Smem<T, D>& sm) {
+// Occupied beacon slots of head h, ascending, into act / *nact.
+__device__ __forceinline__ void active_slots(const Args& a, int h, int* act, int* nact) {
     if (threadIdx.x == 0) {
         const int32_t* cnt = a.counts + (size_t)h * a.C;  // not read when C == 0
         int n = 0;
         for (int c = 0; c < a.C; ++c)
-            if (cnt[c] > 0) sm.act[n++] = c;
-        sm.nact = n;
+            if (cnt[c] > 0) act[n++] = c;
+        *nact = n;
     }
     __syncthreads();
 }
 
-// Observation rows [r0, r0 + nr) of head h into LDS: rows below nact are
-// the occupied beacons rotated to the step and rounded to the cache dtype,
-// then the G*W recent queries (contiguous in q_win), then zero padding.
-template <typename T, int D>
-__device__ void build_rows(const Args& a, int h, int r0, int nr, Smem<T, D>& sm) {
-    constexpr int LD = D + Tr<T>::PAD;
+// Observation rows [r0, r0 + nr) of head h into LDS rows of stride LD: rows
+// below nact are the occupied beacons rotated to the step and rounded to the
+// cache dtype, then the G*W recent queries (contiguous in q_win), then zero
+// padding.
+template <typename T, int D, int LD>
+__device__ void build_rows(const Args& a, int h, int r0, int nr, const int* act, int nact, T* y) {
     constexpr int VPR = D * Tr<T>::ES / 16;
     const int tid = threadIdx.x;
     const int b = h / a.Hkv, kh = h % a.Hkv;
-    const int nact = sm.nact, R = nact + a.G * a.W;
+    const int R = nact + a.G * a.W;
     // beacon rows in this group
     const int bl = max(0, min(nact, r0 + nr) - r0);
     for (int idx = tid; idx < bl * (D / 2); idx += kThreads) {
         const int r = idx / (D / 2), i = idx % (D / 2);
-        const float* beta = a.beacons + ((size_t)h * a.C + sm.act[r0 + r]) * D;
+        const float* beta = a.beacons + ((size_t)h * a.C + act[r0 + r]) * D;
         float2 p = make_float2(beta[i], beta[i + D / 2]);
         if (a.rope_cos) p = rope_pair(p.x, p.y, a.rope_cos[i], a.rope_sin[i]);
-        sm.y[r * LD + i] = to_elem<T>(p.x);
-        sm.y[r * LD + i + D / 2] = to_elem<T>(p.y);
+        y[r * LD + i] = to_elem<T>(p.x);
+        y[r * LD + i + D / 2] = to_elem<T>(p.y);
     }
     // recent rows and padding, 16 bytes at a time
     const T* q = reinterpret_cast<const T*>(a.qwin) + ((size_t)b * a.Hq + (size_t)kh * a.G) * a.W * D;
@@ -212,18 +227,85 @@ __device__ void build_rows(const Args& a, int h, int r0, int nr, Smem<T, D>& sm)
         const int gr = r0 + r;  // row index within the head
         dev::u32x4 val = {0u, 0u, 0u, 0u};
         if (gr < R) val = reinterpret_cast<const dev::u32x4*>(q + (size_t)(gr - nact) * D)[v];
-        *reinterpret_cast<dev::u32x4*>(sm.y + r * LD + v * (16 / Tr<T>::ES)) = val;
+        *reinterpret_cast<dev::u32x4*>(y + r * LD + v * (16 / Tr<T>::ES)) = val;
     }
 }
 
+// Fold a head's chunk statistics into lse (called by the head's last S item)
+// and publish it.
+__device__ void fold_and_publish(const Args& a, int h, const int* act, int nact, int* hc) {
+    const int tid = threadIdx.x;
+    const int R = nact + a.G * a.W;
+    const size_t hb = (size_t)h * a.nch * a.R_pad_max;
+    for (int r = tid; r < a.R_pad_max; r += kThreads) {
+        float mm = -INFINITY, zz = 0.f;
+        if (r < R) {
+            // eight chunks' statistics in flight at once: these are memory
+            // round trips on the head's critical path
+            for (int c0 = 0; c0 < a.nch; c0 += 8) {
+                float pm[8], pz[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const size_t i = hb + (size_t)min(c0 + u, a.nch - 1) * a.R_pad_max + r;
+                    pm[u] = dev::ld_coherent(a.part_m + i);
+                    pz[u] = dev::ld_coherent(a.part_z + i);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (c0 + u < a.nch) merge_mz(mm, zz, pm[u], pz[u]);
+            }
+        }
+        const float l2 = (r < R) ? mm + log2f(zz) : INFINITY;  // padding rows never win
+        dev::st_coherent(a.lse2 + (size_t)h * a.R_pad_max + r, l2);
+        if (a.row_lse && r < R) {
+            const int slot = (r < nact) ? act[r] : a.C + (r - nact);
+            a.row_lse[(size_t)h * (a.C + a.G * a.W) + slot] = l2 * 0.69314718055994531f;
+        }
+    }
+    if (a.row_lse) {  // empty beacon slots have no row
+        const int32_t* cnt = a.counts + (size_t)h * a.C;
+        for (int c = tid; c < a.C; c += kThreads)
+            if (cnt[c] <= 0) a.row_lse[(size_t)h * (a.C + a.G * a.W) + c] = -INFINITY;
+    }
+    dev::wait_all_memory();
+    __syncthreads();
+    if (tid == 0) dev::st_flag(hc + kHcReady, 1);
+}
+
+// Publish this S item's statistics; the head's last S item folds them.
+__device__ __forceinline__ void publish_stats(const Args& a, int h, const int* act, int nact, int* s_flag) {
+    dev::wait_all_memory();  // statistics stored before the counter moves
+    __syncthreads();
+    int* hc = a.hctl + (size_t)h * kHcWords;
+    if (threadIdx.x == 0) *s_flag = (dev::fetch_add_relaxed(hc + kHcP1Count, 1) == a.nch - 1);
+    __syncthreads();
+    if (*s_flag) fold_and_publish(a, h, act, nact, hc);
+}
+
+// Block until the head's lse is published (one thread waits, then all).
+__device__ __forceinline__ bool await_lse(const Args& a, int h, int* s_flag) {
+    if (threadIdx.x == 0) {
+        *s_flag = dev::wait_flag(a.hctl + (size_t)h * kHcWords + kHcReady);
+        if (!*s_flag) dev::raise_error(a.hdr, kErrScoreWait);
+    }
+    __syncthreads();
+    return *s_flag != 0;
+}
+
 // ---- S(h, chunk): row statistics over one key chunk -------------------------
+//
+// Wave w takes keys [kw, kw + 64*KGN) in groups of 64 (four 16-key tiles).
+// MFMA rows are keys and columns observation rows, so a lane owns one row
+// (lane & 15 within the tile) and 16 keys of each group.  Keys at or past N
+// enter with the accumulator seeded at -inf, so they add exp2(-inf) = 0 and
+// need no per-element masking.
 template <typename T, int D, int KGN>
 __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int* s_flag) {
     constexpr int RG = Tr<T>::RG, LD = D + Tr<T>::PAD, RTM = RG / 16;
     constexpr int KC = kWaves * 64 * KGN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    active_slots<T, D>(a, h, sm);
+    active_slots(a, h, sm.act, &sm.nact);
     const int nact = sm.nact;
     const int R = nact + a.G * a.W;
     const int Rp = (R + 15) & ~15;
@@ -236,7 +318,7 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     for (int r0 = 0; r0 < Rp; r0 += RG) {
         const int nr = min(RG, Rp - r0), RT = nr / 16;
         __syncthreads();
-        build_rows<T, D>(a, h, r0, nr, sm);
+        build_rows<T, D, LD>(a, h, r0, nr, sm.act, nact, sm.y);
         __syncthreads();
         float m[RTM], z[RTM];
 #pragma unroll
@@ -244,43 +326,42 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             m[i] = -INFINITY;
             z[i] = 0.f;
         }
-#pragma unroll
-        for (int kg = 0; kg < KGN; ++kg) {
+        const int ngroups = max(0, min(KGN, (N - kw + 63) / 64));
+#pragma unroll 1
+        for (int kg = 0; kg < ngroups; ++kg) {
             const int kb = kw + kg * 64;
-            if (kb < N) {
-                Op<T, D> kop[4];
+            Op<T, D> kop[4];
+            load_group<T, D>(kop, Kh, kb, N, c16, g);
+            f32x4 seed[4];  // 0 for keys below N, -inf past it
 #pragma unroll
-                for (int t = 0; t < 4; ++t) load_key_tile<T, D>(kop[t], Kh, min(kb + t * 16 + c16, N - 1), g);
+            for (int t = 0; t < 4; ++t)
 #pragma unroll
-                for (int rt = 0; rt < RTM; ++rt) {
-                    if (rt < RT) {
-                        Op<T, D> yop;
-                        load_row_tile<T, D>(yop, sm.y + (rt * 16 + c16) * LD + g * Op<T, D>::SL);
-                        f32x4 acc[4];
-                        float gm = -INFINITY;
+                for (int v = 0; v < 4; ++v) seed[t][v] = (kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
 #pragma unroll
-                        for (int t = 0; t < 4; ++t) {
-                            acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-                            mma(acc[t], kop[t], yop);  // rows = keys, columns = observation rows
+            for (int rt = 0; rt < RTM; ++rt) {
+                if (rt < RT) {
+                    Op<T, D> yop;
+                    load_row_tile<T, D>(yop, sm.y + (rt * 16 + c16) * LD, g);
+                    f32x4 acc[4];
 #pragma unroll
-                            for (int v = 0; v < 4; ++v) {
-                                const int key = kb + t * 16 + 4 * g + v;
-                                float x = (key < N) ? acc[t][v] : -INFINITY;
-                                acc[t][v] = x;
-                                gm = fmaxf(gm, x);
-                            }
-                        }
-                        const float mnew = fmaxf(m[rt], gm * s2);
-                        if (mnew != -INFINITY) {
-                            float zz = (m[rt] == -INFINITY) ? 0.f : z[rt] * fast_exp2(m[rt] - mnew);
-#pragma unroll
-                            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                                for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(acc[t][v], s2, -mnew));
-                            z[rt] = zz;
-                            m[rt] = mnew;
-                        }
+                    for (int t = 0; t < 4; ++t) {
+                        acc[t] = seed[t];
+                        mma(acc[t], kop[t], yop);  // rows = keys, columns = observation rows
                     }
+                    float gm = fmaxf(fmaxf(acc[0][0], acc[0][1]), fmaxf(acc[0][2], acc[0][3]));
+#pragma unroll
+                    for (int t = 1; t < 4; ++t)
+                        gm = fmaxf(gm, fmaxf(fmaxf(acc[t][0], acc[t][1]), fmaxf(acc[t][2], acc[t][3])));
+                    const float mnew = fmaxf(m[rt], gm * s2);
+                    // a lane may see no valid key yet: keep its sums at 0, not NaN
+                    const float ms = (mnew == -INFINITY) ? 0.f : mnew;
+                    float zz = z[rt] * fast_exp2(m[rt] - ms);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(acc[t][v], s2, -ms));
+                    z[rt] = zz;
+                    m[rt] = mnew;
                 }
             }
         }
@@ -305,179 +386,447 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             dev::st_coherent(a.part_z + pbase + r0 + r, zz);
         }
     }
-    // publish: statistics stored before the counter moves
-    dev::wait_all_memory();
-    __syncthreads();
-    if (tid == 0) *s_flag = (dev::fetch_add_relaxed(a.p1cnt + h, 1) == a.nch - 1);
-    __syncthreads();
-    if (!*s_flag) return;
-    // last chunk of the head: fold the chunk statistics into lse
-    const size_t hb = (size_t)h * a.nch * a.R_pad_max;
-    for (int r = tid; r < Rp; r += kThreads) {
-        float mm = -INFINITY, zz = 0.f;
-        if (r < R)
-            for (int c = 0; c < a.nch; ++c) {
-                const size_t i = hb + (size_t)c * a.R_pad_max + r;
-                merge_mz(mm, zz, dev::ld_coherent(a.part_m + i), dev::ld_coherent(a.part_z + i));
-            }
-        const float l2 = (r < R) ? mm + log2f(zz) : INFINITY;  // padding rows never win
-        dev::st_coherent(a.lse2 + (size_t)h * a.R_pad_max + r, l2);
-        if (a.row_lse && r < R) {
-            const int slot = (r < nact) ? sm.act[r] : a.C + (r - nact);
-            a.row_lse[(size_t)h * (a.C + a.G * a.W) + slot] = l2 * 0.69314718055994531f;
-        }
-    }
-    if (a.row_lse) {  // empty beacon slots have no row
-        const int32_t* cnt = a.counts + (size_t)h * a.C;
-        for (int c = tid; c < a.C; c += kThreads)
-            if (cnt[c] <= 0) a.row_lse[(size_t)h * (a.C + a.G * a.W) + c] = -INFINITY;
-    }
-    dev::wait_all_memory();
-    __syncthreads();
-    if (tid == 0) dev::st_flag(a.ready + h, 1);
+    publish_stats(a, h, sm.act, nact, s_flag);
 }
 
 // ---- F(h, chunk): final max-aggregated scores over one key chunk ----------
+//
+// MFMA rows are observation rows and columns keys; the accumulator starts at
+// -lse2_r / s2, so each output is (l_rj - lse_r) / (s2 ln 2) and a key's
+// score is the max down its column.  Per-key maxima collect in LDS (across
+// row groups) and are written out coalesced at the end.
 template <typename T, int D, int KGN>
-__device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm) {
+__device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int* s_flag) {
     constexpr int RG = Tr<T>::RG, LD = D + Tr<T>::PAD, RTM = RG / 16;
     constexpr int KC = kWaves * 64 * KGN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    active_slots<T, D>(a, h, sm);
+    if (!await_lse(a, h, s_flag)) return;
+    active_slots(a, h, sm.act, &sm.nact);
     const int R = sm.nact + a.G * a.W;
     const int Rp = (R + 15) & ~15;
     const T* Kh = reinterpret_cast<const T*>(a.K) + (size_t)h * a.N_cap * D;
-    const int kw = chunk * KC + wave * 64 * KGN;
+    const int k0 = chunk * KC;
+    const int kw = k0 + wave * 64 * KGN;
     const int N = a.N;
     const float inv_s2 = 1.0f / a.s2;
-
-    float best[4 * KGN];
-#pragma unroll
-    for (int i = 0; i < 4 * KGN; ++i) best[i] = -INFINITY;
+    for (int i = tid; i < KC; i += kThreads) sm.best[i] = -INFINITY;
+    const int ngroups = max(0, min(KGN, (N - kw + 63) / 64));
 
     for (int r0 = 0; r0 < Rp; r0 += RG) {
         const int nr = min(RG, Rp - r0), RT = nr / 16;
         __syncthreads();
-        build_rows<T, D>(a, h, r0, nr, sm);
+        build_rows<T, D, LD>(a, h, r0, nr, sm.act, sm.nact, sm.y);
         for (int r = tid; r < nr; r += kThreads)
             sm.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r0 + r) * inv_s2;
         __syncthreads();
-#pragma unroll
-        for (int kg = 0; kg < KGN; ++kg) {
+#pragma unroll 1
+        for (int kg = 0; kg < ngroups; ++kg) {
             const int kb = kw + kg * 64;
-            if (kb < N) {
-                Op<T, D> kop[4];
+            Op<T, D> kop[4];
+            load_group<T, D>(kop, Kh, kb, N, c16, g);
+            float best[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
-                for (int t = 0; t < 4; ++t) load_key_tile<T, D>(kop[t], Kh, min(kb + t * 16 + c16, N - 1), g);
+            for (int rt = 0; rt < RTM; ++rt) {
+                if (rt < RT) {
+                    Op<T, D> yop;
+                    load_row_tile<T, D>(yop, sm.y + (rt * 16 + c16) * LD, g);
+                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(sm.nlse + rt * 16 + 4 * g);
 #pragma unroll
-                for (int rt = 0; rt < RTM; ++rt) {
-                    if (rt < RT) {
-                        Op<T, D> yop;
-                        load_row_tile<T, D>(yop, sm.y + (rt * 16 + c16) * LD + g * Op<T, D>::SL);
-                        const f32x4 c0 = *reinterpret_cast<const f32x4*>(sm.nlse + rt * 16 + 4 * g);
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) {
-                            f32x4 acc = c0;
-                            mma(acc, yop, kop[t]);  // rows = observation rows, columns = keys
-                            best[kg * 4 + t] =
-                                fmaxf(best[kg * 4 + t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
-                        }
+                    for (int t = 0; t < 4; ++t) {
+                        f32x4 acc = c0;
+                        mma(acc, yop, kop[t]);  // rows = observation rows, columns = keys
+                        best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
                     }
                 }
             }
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                float b = best[t];
+                b = fmaxf(b, dev::shfl_xor_f(b, 16));
+                b = fmaxf(b, dev::shfl_xor_f(b, 32));
+                float* slot = sm.best + (kb - k0) + t * 16 + c16;  // this wave's own keys
+                if (g == t) *slot = fmaxf(*slot, b);
+            }
         }
     }
+    __syncthreads();
     float* out = a.scores + (size_t)h * N;
+    for (int i = tid; i < KC; i += kThreads)
+        if (k0 + i < N) out[k0 + i] = sm.best[i] * a.s2ln2;
+}
+
+// Workgroup -> head.  The grid lists, for s = 0, 1, ..., nch workgroups of
+// head s (if s < P) and then nch workgroups of head s - lag (if s >= lag),
+// so each head's second half starts about `lag` heads after its first.
+__device__ __forceinline__ int head_of_block(const Args& a, int b) {
+    const int P = a.P, nch = a.nch, L = a.lag;
+    if (b < L * nch) return b / nch;
+    b -= L * nch;
+    if (b < (P - L) * 2 * nch) {
+        const int s = L + b / (2 * nch);
+        return (b % (2 * nch) < nch) ? s : s - L;
+    }
+    b -= (P - L) * 2 * nch;
+    return P - L + b / nch;
+}
+
+// ---- fast path: bf16 cache, at most 144 observation rows -----------------
+//
+// Key tiles are staged through LDS with coalesced global_load_lds_dwordx4
+// (direct to LDS, no registers), double-buffered per wave so the next group
+// of 32 keys is in flight while this one is computed; a 16-lane ds_read_b128
+// of a staged tile is conflict-free thanks to an XOR swizzle of the 16-byte
+// chunks of each key row.  The observation rows (at most 144) are held in
+// registers for the whole item, so they cost no LDS traffic in the loop.
+//
+// The two stages are distinct __shared__ variables and the key loop is
+// unrolled by two, so every LDS read names one stage; the compiler then
+// waits only for the loads into that stage, not for the group in flight
+// into the other one.
+constexpr int kFRT = 9;   // row tiles kept in registers
+constexpr int kFKG = 32;  // keys per group: two 16-key tiles
+
+template <int D>
+struct KeyStage {
+    static constexpr int CPR = D * 2 / 16;       // 16-byte chunks per key row
+    static constexpr int RPI = 64 / CPR;         // key rows per load instruction
+    static constexpr int NI = kFKG / RPI;        // load instructions per group
+    static constexpr int ELEMS = kFKG * D;       // bf16 elements per group
+    static constexpr int ROW_LD = D + 8;         // row stride of the observation rows
+    static constexpr int ROW_ELEMS = kFRT * 16 * ROW_LD;
+    // chunk position of logical chunk c of row r is c ^ swz(r)
+    __device__ static int swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+};
+
+template <int D>
+struct alignas(16) StageA {
+    uint16_t k[kWaves][KeyStage<D>::ELEMS];
+};
+template <int D>
+struct alignas(16) StageB {  // the observation rows are built here first
+    static constexpr int KE = kWaves * KeyStage<D>::ELEMS, RE = KeyStage<D>::ROW_ELEMS;
+    uint16_t e[KE > RE ? KE : RE];
+    __device__ uint16_t* k(int wave) { return e + wave * KeyStage<D>::ELEMS; }
+};
+
+template <int D>
+struct alignas(16) FastSmem {
+    union {
+        struct {
+            float m[kWaves][kFRT * 16];
+            float z[kWaves][kFRT * 16];
+        } red;                          // S items: per-wave row statistics
+        float best[kWaves * 256];       // F items: per-key maxima of the chunk
+    } v;
+    float nlse[kFRT * 16];
+    int act[kMaxC];
+    int nact;
+};
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Start loading keys [kb, kb + 32) of the head into a wave's stage.  Load
+// instruction j writes 1 KB contiguous at stage + 1 KB * j, lane l's 16
+// bytes at offset 16 l: key row r = j*RPI + l / CPR, swizzled position
+// l % CPR, which holds logical chunk (l % CPR) ^ swz(r).  Each group of CPR
+// lanes reads one whole key row.  Keys past N read key N - 1.
+template <int D>
+__device__ __forceinline__ void issue_group(const uint16_t* Kh, int kb, int N, uint16_t* stage, int lane) {
+    using KS = KeyStage<D>;
+    const int rs = lane / KS::CPR, cs = lane % KS::CPR;
 #pragma unroll
-    for (int i = 0; i < 4 * KGN; ++i) {
-        float b = best[i];
+    for (int j = 0; j < KS::NI; ++j) {
+        const int r = j * KS::RPI + rs;
+        const uint16_t* src = Kh + (size_t)min(kb + r, N - 1) * D + ((cs ^ KS::swz(r)) * 8);
+        __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(stage + j * 512), 16, 0,
+                                         0);
+    }
+}
+
+// MFMA operand of staged key tile t for lane (c16, g): vector v holds
+// logical chunk 4 v + g of key row 16 t + c16.
+template <int D>
+__device__ __forceinline__ void read_key_tile(Op<uint16_t, D>& op, const uint16_t* stage, int t, int c16, int g) {
+    using KS = KeyStage<D>;
+    const int r = t * 16 + c16;
+    const uint16_t* row = stage + r * D;
+#pragma unroll
+    for (int v = 0; v < Op<uint16_t, D>::NV; ++v)
+        op.v[v] = *reinterpret_cast<const dev::u32x4*>(row + ((4 * v + g) ^ KS::swz(r)) * 8);
+}
+
+// Build this head's rows in LDS (in stage B, which holds no keys yet) and
+// copy them into registers; every wave holds all of them.  Afterwards
+// stage B may be overwritten.
+template <int D>
+__device__ __forceinline__ int rows_to_registers(const Args& a, int h, FastSmem<D>& sm, StageB<D>& sb,
+                                                 Op<uint16_t, D>* yr, int c16, int g) {
+    constexpr int LD = KeyStage<D>::ROW_LD;
+    active_slots(a, h, sm.act, &sm.nact);
+    const int R = sm.nact + a.G * a.W, Rp = (R + 15) & ~15;
+    build_rows<uint16_t, D, LD>(a, h, 0, Rp, sm.act, sm.nact, sb.e);
+    __syncthreads();
+#pragma unroll
+    for (int rt = 0; rt < kFRT; ++rt)
+        if (rt < Rp / 16) load_row_tile<uint16_t, D>(yr[rt], sb.e + (rt * 16 + c16) * LD, g);
+    __syncthreads();  // every wave holds its rows: stage B may now take keys
+    return Rp / 16;
+}
+
+// Running (max, sum) of one S item over one staged group of 32 keys.
+template <int D>
+__device__ __forceinline__ void stats_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr, int RT,
+                                            float s2, float* m, float* z, int c16, int g) {
+    Op<uint16_t, D> kop[2];
+    read_key_tile<D>(kop[0], st, 0, c16, g);
+    read_key_tile<D>(kop[1], st, 1, c16, g);
+    f32x4 seed[2];  // 0 for keys below N, -inf past it
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) seed[t][v] = (kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
+#pragma unroll
+    for (int rt = 0; rt < kFRT; ++rt) {
+        if (rt < RT) {
+            f32x4 acc[2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                acc[t] = seed[t];
+                mma(acc[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
+            }
+            const float gm = fmaxf(fmaxf(fmaxf(acc[0][0], acc[0][1]), fmaxf(acc[0][2], acc[0][3])),
+                                   fmaxf(fmaxf(acc[1][0], acc[1][1]), fmaxf(acc[1][2], acc[1][3])));
+            const float mnew = fmaxf(m[rt], gm * s2);
+            const float ms = (mnew == -INFINITY) ? 0.f : mnew;  // no valid key yet: sums stay 0
+            float zz = z[rt] * fast_exp2(m[rt] - ms);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(acc[t][v], s2, -ms));
+            z[rt] = zz;
+            m[rt] = mnew;
+        }
+    }
+}
+
+// Per-key maxima of one F item over one staged group of 32 keys.
+template <int D>
+__device__ __forceinline__ void final_group(const uint16_t* st, int kofs, const Op<uint16_t, D>* yr, int RT,
+                                            const float* nlse, float* best_out, int c16, int g) {
+    Op<uint16_t, D> kop[2];
+    read_key_tile<D>(kop[0], st, 0, c16, g);
+    read_key_tile<D>(kop[1], st, 1, c16, g);
+    float best[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+    for (int rt = 0; rt < kFRT; ++rt) {
+        if (rt < RT) {
+            const f32x4 c0 = *reinterpret_cast<const f32x4*>(nlse + rt * 16 + 4 * g);
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                f32x4 acc = c0;
+                mma(acc, yr[rt], kop[t]);  // rows = observation rows, columns = keys
+                best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
+            }
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        float b = best[t];
         b = fmaxf(b, dev::shfl_xor_f(b, 16));
         b = fmaxf(b, dev::shfl_xor_f(b, 32));
-        const int key = kw + (i >> 2) * 64 + (i & 3) * 16 + c16;
-        if (g == (i & 3) && key < N) out[key] = b * a.s2ln2;
+        if (g == t) best_out[kofs + t * 16 + c16] = b;
     }
 }
 
-// Ticket -> work item.  kind 1 = S, 2 = F.  The S items of head h come
-// `lag` heads before its F items.
-__device__ __forceinline__ void decode(const Args& a, int t, int& kind, int& h, int& c) {
-    const int P = a.P, nch = a.nch, L = a.lag;
-    if (t < L * nch) {
-        kind = 1;
-        h = t / nch;
-        c = t % nch;
-        return;
+// Wait until the group read next has landed in this wave's stage; `more`
+// says whether the following group is still in flight behind it.
+template <int D>
+__device__ __forceinline__ void wait_group(bool more) {
+    if (more)
+        wait_vmem<KeyStage<D>::NI>();
+    else
+        wait_vmem<0>();
+}
+
+template <int D, int GPW>
+__device__ void fast_stats(const Args& a, int h, int chunk, FastSmem<D>& sm, StageA<D>& sa, StageB<D>& sb,
+                           int* s_flag) {
+    constexpr int KPW = GPW * kFKG, KC = kWaves * KPW;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    const uint16_t* Kh = reinterpret_cast<const uint16_t*>(a.K) + (size_t)h * a.N_cap * D;
+    const int N = a.N;
+    const int kw = chunk * KC + wave * KPW;
+    const int ngroups = max(0, min(GPW, (N - kw + kFKG - 1) / kFKG));
+    uint16_t* stA = sa.k[wave];
+    uint16_t* stB = sb.k(wave);
+    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);  // in flight while the rows are built
+    Op<uint16_t, D> yr[kFRT];
+    const int RT = rows_to_registers<D>(a, h, sm, sb, yr, c16, g);
+    if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+    const float s2 = a.s2;
+    float m[kFRT], z[kFRT];
+#pragma unroll
+    for (int i = 0; i < kFRT; ++i) {
+        m[i] = -INFINITY;
+        z[i] = 0.f;
     }
-    t -= L * nch;
-    if (t < (P - L) * 2 * nch) {
-        const int s = L + t / (2 * nch), r = t % (2 * nch);
-        if (r < nch) {
-            kind = 1;
-            h = s;
-            c = r;
-        } else {
-            kind = 2;
-            h = s - L;
-            c = r - nch;
+#pragma unroll 1
+    for (int kg = 0; kg < ngroups; kg += 2) {
+        const int kb = kw + kg * kFKG;
+        wait_group<D>(kg + 1 < ngroups);
+        stats_group<D>(stA, kb, N, yr, RT, s2, m, z, c16, g);
+        if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
+        if (kg + 1 < ngroups) {
+            wait_group<D>(kg + 2 < ngroups);
+            stats_group<D>(stB, kb + kFKG, N, yr, RT, s2, m, z, c16, g);
+            if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
         }
-        return;
     }
-    t -= (P - L) * 2 * nch;
-    kind = 2;
-    h = P - L + t / nch;
-    c = t % nch;
+    // lanes sharing a row: g = 0..3, then waves
+#pragma unroll
+    for (int rt = 0; rt < kFRT; ++rt) {
+        if (rt < RT) {
+            merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 16), dev::shfl_xor_f(z[rt], 16));
+            merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 32), dev::shfl_xor_f(z[rt], 32));
+            if (g == 0) {
+                sm.v.red.m[wave][rt * 16 + c16] = m[rt];
+                sm.v.red.z[wave][rt * 16 + c16] = z[rt];
+            }
+        }
+    }
+    __syncthreads();
+    const size_t pbase = ((size_t)h * a.nch + chunk) * a.R_pad_max;
+    for (int r = tid; r < RT * 16; r += kThreads) {
+        float mm = sm.v.red.m[0][r], zz = sm.v.red.z[0][r];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) merge_mz(mm, zz, sm.v.red.m[w][r], sm.v.red.z[w][r]);
+        dev::st_coherent(a.part_m + pbase + r, mm);
+        dev::st_coherent(a.part_z + pbase + r, zz);
+    }
+    publish_stats(a, h, sm.act, sm.nact, s_flag);
 }
 
+template <int D, int GPW>
+__device__ void fast_final(const Args& a, int h, int chunk, FastSmem<D>& sm, StageA<D>& sa, StageB<D>& sb,
+                           int* s_flag) {
+    constexpr int KPW = GPW * kFKG, KC = kWaves * KPW;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    const uint16_t* Kh = reinterpret_cast<const uint16_t*>(a.K) + (size_t)h * a.N_cap * D;
+    const int N = a.N;
+    const int k0 = chunk * KC, kw = k0 + wave * KPW;
+    const int ngroups = max(0, min(GPW, (N - kw + kFKG - 1) / kFKG));
+    uint16_t* stA = sa.k[wave];
+    uint16_t* stB = sb.k(wave);
+    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);  // in flight while lse is awaited
+    if (!await_lse(a, h, s_flag)) {
+        wait_vmem<0>();  // no load may land in LDS after this workgroup ends
+        return;
+    }
+    Op<uint16_t, D> yr[kFRT];
+    const float inv_s2 = 1.0f / a.s2;
+    for (int r = tid; r < kFRT * 16; r += kThreads)
+        sm.nlse[r] = (r < a.R_pad_max) ? -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r) * inv_s2
+                                        : -INFINITY;
+    const int RT = rows_to_registers<D>(a, h, sm, sb, yr, c16, g);
+    if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+    const int kofs = wave * KPW;  // this wave's keys within the chunk
+#pragma unroll 1
+    for (int kg = 0; kg < ngroups; kg += 2) {
+        wait_group<D>(kg + 1 < ngroups);
+        final_group<D>(stA, kofs + kg * kFKG, yr, RT, sm.nlse, sm.v.best, c16, g);
+        if (kg + 2 < ngroups) issue_group<D>(Kh, kw + (kg + 2) * kFKG, N, stA, lane);
+        if (kg + 1 < ngroups) {
+            wait_group<D>(kg + 2 < ngroups);
+            final_group<D>(stB, kofs + (kg + 1) * kFKG, yr, RT, sm.nlse, sm.v.best, c16, g);
+            if (kg + 3 < ngroups) issue_group<D>(Kh, kw + (kg + 3) * kFKG, N, stB, lane);
+        }
+    }
+    __syncthreads();
+    float* out = a.scores + (size_t)h * N;
+    for (int i = tid; i < KC; i += kThreads)
+        if (k0 + i < N) out[k0 + i] = sm.v.best[i] * a.s2ln2;
+}
+
+// ---- kernel entry, shared by both paths ------------------------------------
+struct NoStage {
+    int unused;
+};
 template <typename T, int D, int KGN>
-__global__ __launch_bounds__(kThreads) void score_kernel(Args a) {
-    __shared__ Smem<T, D> sm;
+struct GenericPath {
+    using Shared = Smem<T, D>;
+    using SA = NoStage;
+    using SB = NoStage;
+    __device__ static void stats(const Args& a, int h, int c, Shared& sm, SA&, SB&, int* f) {
+        stats_item<T, D, KGN>(a, h, c, sm, f);
+    }
+    __device__ static void final(const Args& a, int h, int c, Shared& sm, SA&, SB&, int* f) {
+        final_item<T, D, KGN>(a, h, c, sm, f);
+    }
+};
+template <int D, int GPW>
+struct FastPath {
+    using Shared = FastSmem<D>;
+    using SA = StageA<D>;
+    using SB = StageB<D>;
+    __device__ static void stats(const Args& a, int h, int c, Shared& sm, SA& sa, SB& sb, int* f) {
+        fast_stats<D, GPW>(a, h, c, sm, sa, sb, f);
+    }
+    __device__ static void final(const Args& a, int h, int c, Shared& sm, SA& sa, SB& sb, int* f) {
+        fast_final<D, GPW>(a, h, c, sm, sa, sb, f);
+    }
+};
+
+template <class Path>
+__global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
+    __shared__ typename Path::Shared sm;
+    __shared__ typename Path::SA sa;
+    __shared__ typename Path::SB sb;
     __shared__ int s_ticket, s_ok, s_flag;
     const int tid = threadIdx.x;
+    const int h = head_of_block(a, blockIdx.x);
+    int* hc = a.hctl + (size_t)h * kHcWords;
     if (tid == 0) {
         s_ok = dev::stamp_ok(a.hdr, a.P, a.budget);
         if (s_ok)
-            s_ticket = dev::fetch_add_relaxed(a.hdr + kHdrScTicket, 1);
+            s_ticket = dev::fetch_add_relaxed(hc + kHcScTicket, 1);
         else
             dev::raise_error(a.hdr, kErrStamp);
     }
     __syncthreads();
     if (!s_ok) return;
-    if (s_ticket >= a.total) {  // control block was not clear: do nothing
+    if (s_ticket >= 2 * a.nch) {  // control block was not clear: do nothing
         if (tid == 0) dev::raise_error(a.hdr, kErrStamp);
         return;
     }
-    int kind, h, c;
-    decode(a, s_ticket, kind, h, c);
-    if (kind == 1) {
-        stats_item<T, D, KGN>(a, h, c, sm, &s_flag);
-    } else {
-        if (tid == 0) {
-            s_flag = dev::wait_flag(a.ready + h);
-            if (!s_flag) dev::raise_error(a.hdr, kErrScoreWait);
-        }
-        __syncthreads();
-        if (s_flag) final_item<T, D, KGN>(a, h, c, sm);
-    }
-    // The last item to finish clears the control block for the next launch.
+    if (s_ticket < a.nch)
+        Path::stats(a, h, s_ticket, sm, sa, sb, &s_flag);
+    else
+        Path::final(a, h, s_ticket - a.nch, sm, sa, sb, &s_flag);
+    // The head's last workgroup to finish clears its control words.
     __syncthreads();
-    if (tid == 0) s_flag = (dev::fetch_add_relaxed(a.hdr + kHdrScDone, 1) == a.total - 1);
+    if (tid == 0) s_flag = (dev::fetch_add_relaxed(hc + kHcScDone, 1) == 2 * a.nch - 1);
     __syncthreads();
-    if (s_flag) {
-        for (int i = tid; i < a.P; i += kThreads) {
-            dev::st_flag(a.p1cnt + i, 0);
-            dev::st_flag(a.ready + i, 0);
-        }
-        if (tid == 0) {
-            dev::st_flag(a.hdr + kHdrScTicket, 0);
-            dev::st_flag(a.hdr + kHdrScDone, 0);
-        }
+    if (s_flag && tid == 0) {
+        dev::st_flag(hc + kHcScTicket, 0);
+        dev::st_flag(hc + kHcScDone, 0);
+        dev::st_flag(hc + kHcP1Count, 0);
+        dev::st_flag(hc + kHcReady, 0);
     }
 }
 
-template <typename T, int D, int KGN>
+template <class Path>
 hipError_t launch_t(const Args& a, hipStream_t s) {
-    hipLaunchKernelGGL((score_kernel<T, D, KGN>), dim3(a.total), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((score_kernel<Path>), dim3(a.total), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
@@ -498,8 +847,7 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
     a.scores = scores;
     a.row_lse = row_lse;
     a.hdr = reinterpret_cast<int*>(w);
-    a.p1cnt = reinterpret_cast<int*>(w + L.p1cnt);
-    a.ready = reinterpret_cast<int*>(w + L.ready);
+    a.hctl = reinterpret_cast<int*>(w + L.hctl);
     a.part_m = reinterpret_cast<float*>(w + L.part_m);
     a.part_z = reinterpret_cast<float*>(w + L.part_z);
     a.lse2 = reinterpret_cast<float*>(w + L.lse2);
@@ -527,10 +875,15 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
     a.s2 = sc * 1.4426950408889634f;
     a.s2ln2 = a.s2 * 0.69314718055994531f;
     const bool bf = d.dtype == BKV_BF16;
-    if (bf && d.D == 128) return L.kgn == 4 ? launch_t<uint16_t, 128, 4>(a, s) : launch_t<uint16_t, 128, 1>(a, s);
-    if (bf && d.D == 64) return L.kgn == 4 ? launch_t<uint16_t, 64, 4>(a, s) : launch_t<uint16_t, 64, 1>(a, s);
-    if (d.D == 128) return L.kgn == 4 ? launch_t<float, 128, 4>(a, s) : launch_t<float, 128, 1>(a, s);
-    return L.kgn == 4 ? launch_t<float, 64, 4>(a, s) : launch_t<float, 64, 1>(a, s);
+    const bool k4 = L.kgn == 4;  // 1024-key items (else 256)
+    if (bf && L.R_pad_max <= kFRT * 16) {  // all rows fit in registers
+        if (d.D == 128) return k4 ? launch_t<FastPath<128, 8>>(a, s) : launch_t<FastPath<128, 2>>(a, s);
+        return k4 ? launch_t<FastPath<64, 8>>(a, s) : launch_t<FastPath<64, 2>>(a, s);
+    }
+    if (bf && d.D == 128) return k4 ? launch_t<GenericPath<uint16_t, 128, 4>>(a, s) : launch_t<GenericPath<uint16_t, 128, 1>>(a, s);
+    if (bf) return k4 ? launch_t<GenericPath<uint16_t, 64, 4>>(a, s) : launch_t<GenericPath<uint16_t, 64, 1>>(a, s);
+    if (d.D == 128) return k4 ? launch_t<GenericPath<float, 128, 4>>(a, s) : launch_t<GenericPath<float, 128, 1>>(a, s);
+    return k4 ? launch_t<GenericPath<float, 64, 4>>(a, s) : launch_t<GenericPath<float, 64, 1>>(a, s);
 }
 
 }  // namespace bkv

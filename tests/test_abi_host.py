@@ -76,14 +76,14 @@ def test_rows_needed_for_scoring_only():
 
 
 def test_bad_op_and_null_dims():
-    lib = bkv._lib
+    lib = bkv.lib()
     assert bkv.validate(good(), 5) == bkv.ERR_INVALID
     assert lib.bkv_validate(None, 0) == bkv.ERR_INVALID
     assert lib.bkv_workspace_bytes(None, 4) == 0
 
 
 def test_null_pointers_rejected_before_launch():
-    lib = bkv._lib
+    lib = bkv.lib()
     d = good()
     r = ctypes.byref(d)
     assert lib.bkv_score(r, None, None, None, None, None, None, 0.0, None, None, None, 0, None) == bkv.ERR_INVALID
@@ -101,7 +101,7 @@ def test_null_pointers_rejected_before_launch():
 
 
 def test_empty_work_is_a_no_op():
-    lib = bkv._lib
+    lib = bkv.lib()
     for d in (good(B=0), good(N=0)):
         r = ctypes.byref(d)
         assert lib.bkv_score(r, None, None, None, None, None, None, 0.0, None, None, None, 0, None) == bkv.OK
@@ -121,3 +121,11 @@ def test_workspace_sizes():
     assert bkv.workspace_bytes(d2, bkv.OP_COMPACT) == c
     assert bkv.workspace_bytes(d2, bkv.OP_EVICT) > e
     assert bkv.workspace_bytes(good(budget=8192), bkv.OP_COMPACT) > c
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    # no silent fallback: with the library absent the first use raises
+    monkeypatch.setattr(bkv, "_lib", None)
+    monkeypatch.setattr(bkv, "LIB_PATH", os.path.join(ROOT, "no-such-dir", "libbkv.so"))
+    with pytest.raises(ImportError):
+        bkv.validate(good(), bkv.OP_EVICT)
