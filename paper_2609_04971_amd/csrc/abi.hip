@@ -60,6 +60,10 @@ WsLayout ws_layout(const bkv_dims& d) {
     off = align_up(off + sizeof(float) * (size_t)P * L.nch * L.R_pad_max);
     L.lse2 = off;
     off = align_up(off + sizeof(float) * (size_t)P * L.R_pad_max);
+    L.rows = off;
+    off = align_up(off + sizeof(uint16_t) * (size_t)P * L.R_pad_max * d.D);
+    L.rmeta = off;
+    off = align_up(off + sizeof(int32_t) * (size_t)P * kMetaWords);
     L.score_end = off;
     L.scores = off;
     off = align_up(off + sizeof(float) * (size_t)P * d.N);

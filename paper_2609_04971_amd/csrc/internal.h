@@ -40,6 +40,11 @@ enum DevErr : int { kErrScoreWait = 1, kErrCompactWait = 2, kErrStamp = 4, kErrB
 
 constexpr int kSegRows = 64;  // compaction rows per work item
 
+// Per-head row metadata written before scoring: word 0 = number of occupied
+// beacon slots, words kMetaAct.. = those slots, ascending.
+constexpr int kMetaAct = 16;
+constexpr int kMetaWords = 128;
+
 struct WsLayout {
     // control block
     size_t hctl;    // per-head control lines (int32 [P][kHcWords])
@@ -48,6 +53,8 @@ struct WsLayout {
     // data
     size_t part_m, part_z;  // score: per-chunk row statistics (fp32 [P][nch][R_pad_max])
     size_t lse2;            // score: row log2-normalisers (fp32 [P][R_pad_max])
+    size_t rows;            // score: observation rows in MFMA operand order (bf16 [P][R_pad_max][D])
+    size_t rmeta;           // score: per-head occupied-slot list (int32 [P][kMetaWords])
     size_t score_end;
     size_t scores;          // evict: scores when the caller passes none [P][N]
     size_t kept;            // evict: kept indices when the caller passes none [P][budget]

@@ -80,8 +80,10 @@ struct Args {
     float* part_m;  // [P][nch][R_pad_max] chunk row maxima (log2 units)
     float* part_z;  // [P][nch][R_pad_max] chunk row sums relative to part_m
     float* lse2;    // [P][R_pad_max] row log2-normalisers
+    uint16_t* rows; // [P][R_pad_max / 16][NV][64] observation rows, one MFMA operand vector per lane
+    int* rmeta;     // [P][kMetaWords] occupied beacon slots of each head
     int B, Hq, Hkv, G, N, N_cap, W, C, P, budget;
-    int R_pad_max, nch, lag, total;
+    int R_pad_max, nch, key_chunk, lag, total;
     float s2;     // scale * log2(e)
     float s2ln2;  // s2 * ln(2): log2-units-of-raw-dot -> natural log
 };
@@ -240,18 +242,18 @@ __device__ void fold_and_publish(const Args& a, int h, const int* act, int nact,
     for (int r = tid; r < a.R_pad_max; r += kThreads) {
         float mm = -INFINITY, zz = 0.f;
         if (r < R) {
-            // eight chunks' statistics in flight at once: these are memory
+            // sixteen chunks' statistics in flight at once: these are memory
             // round trips on the head's critical path
-            for (int c0 = 0; c0 < a.nch; c0 += 8) {
-                float pm[8], pz[8];
+            for (int c0 = 0; c0 < a.nch; c0 += 16) {
+                float pm[16], pz[16];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
+                for (int u = 0; u < 16; ++u) {
                     const size_t i = hb + (size_t)min(c0 + u, a.nch - 1) * a.R_pad_max + r;
                     pm[u] = dev::ld_coherent(a.part_m + i);
                     pz[u] = dev::ld_coherent(a.part_z + i);
                 }
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
+                for (int u = 0; u < 16; ++u)
                     if (c0 + u < a.nch) merge_mz(mm, zz, pm[u], pz[u]);
             }
         }
@@ -272,14 +274,15 @@ __device__ void fold_and_publish(const Args& a, int h, const int* act, int nact,
     if (tid == 0) dev::st_flag(hc + kHcReady, 1);
 }
 
-// Publish this S item's statistics; the head's last S item folds them.
-__device__ __forceinline__ void publish_stats(const Args& a, int h, const int* act, int nact, int* s_flag) {
+// Count this S item's statistics in; true for the head's last S item, which
+// then folds them.
+__device__ __forceinline__ bool count_stats(const Args& a, int h, int* s_flag) {
     dev::wait_all_memory();  // statistics stored before the counter moves
     __syncthreads();
     int* hc = a.hctl + (size_t)h * kHcWords;
     if (threadIdx.x == 0) *s_flag = (dev::fetch_add_relaxed(hc + kHcP1Count, 1) == a.nch - 1);
     __syncthreads();
-    if (*s_flag) fold_and_publish(a, h, act, nact, hc);
+    return *s_flag != 0;
 }
 
 // Block until the head's lse is published (one thread waits, then all).
@@ -386,7 +389,7 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             dev::st_coherent(a.part_z + pbase + r0 + r, zz);
         }
     }
-    publish_stats(a, h, sm.act, nact, s_flag);
+    if (count_stats(a, h, s_flag)) fold_and_publish(a, h, sm.act, nact, a.hctl + (size_t)h * kHcWords);
 }
 
 // ---- F(h, chunk): final max-aggregated scores over one key chunk ----------
@@ -471,20 +474,69 @@ __device__ __forceinline__ int head_of_block(const Args& a, int b) {
     return P - L + b / nch;
 }
 
+// ---- work-item protocol shared by both paths --------------------------------
+// Take the next work ticket of head h (tickets below nch are S items, the
+// rest F items); false if the workspace stamp or control line is bad.
+__device__ __forceinline__ bool take_ticket(const Args& a, int h, int* s_ticket, int* s_ok) {
+    int* hc = a.hctl + (size_t)h * kHcWords;
+    if (threadIdx.x == 0) {
+        int ok = dev::stamp_ok(a.hdr, a.P, a.budget);
+        if (ok) {
+            const int t = dev::fetch_add_relaxed(hc + kHcScTicket, 1);
+            *s_ticket = t;
+            if (t >= 2 * a.nch) ok = 0;  // control line was not clear: do nothing
+        }
+        if (!ok) dev::raise_error(a.hdr, kErrStamp);
+        *s_ok = ok;
+    }
+    __syncthreads();
+    return *s_ok != 0;
+}
+
+// The head's last workgroup to finish clears its control words.
+__device__ __forceinline__ void finish_item(const Args& a, int h, int* s_flag) {
+    int* hc = a.hctl + (size_t)h * kHcWords;
+    __syncthreads();
+    if (threadIdx.x == 0) *s_flag = (dev::fetch_add_relaxed(hc + kHcScDone, 1) == 2 * a.nch - 1);
+    __syncthreads();
+    if (*s_flag && threadIdx.x == 0) {
+        dev::st_flag(hc + kHcScTicket, 0);
+        dev::st_flag(hc + kHcScDone, 0);
+        dev::st_flag(hc + kHcP1Count, 0);
+        dev::st_flag(hc + kHcReady, 0);
+    }
+}
+
+template <typename T, int D, int KGN>
+__global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
+    __shared__ Smem<T, D> sm;
+    __shared__ int s_ticket, s_ok, s_flag;
+    const int h = head_of_block(a, blockIdx.x);
+    if (!take_ticket(a, h, &s_ticket, &s_ok)) return;
+    if (s_ticket < a.nch)
+        stats_item<T, D, KGN>(a, h, s_ticket, sm, &s_flag);
+    else
+        final_item<T, D, KGN>(a, h, s_ticket - a.nch, sm, &s_flag);
+    finish_item(a, h, &s_flag);
+}
+
 // ---- fast path: bf16 cache, at most 144 observation rows -----------------
 //
-// Key tiles are staged through LDS with coalesced global_load_lds_dwordx4
-// (direct to LDS, no registers), double-buffered per wave so the next group
-// of 32 keys is in flight while this one is computed; a 16-lane ds_read_b128
-// of a staged tile is conflict-free thanks to an XOR swizzle of the 16-byte
-// chunks of each key row.  The observation rows (at most 144) are held in
-// registers for the whole item, so they cost no LDS traffic in the loop.
+// A small kernel first writes each head's observation rows to the workspace
+// in MFMA operand order, so that a work item loads them straight into
+// registers with coalesced 16-byte loads, issued before its ticket returns;
+// they stay in registers for the whole item.  Key tiles are staged through
+// LDS with coalesced global_load_lds_dwordx4 (direct to LDS, no registers),
+// double-buffered per wave so the next group of 32 keys is in flight while
+// this one is computed; a 16-lane ds_read_b128 of a staged tile is
+// conflict-free thanks to an XOR swizzle of the 16-byte chunks of each key
+// row.
 //
 // The two stages are distinct __shared__ variables and the key loop is
 // unrolled by two, so every LDS read names one stage; the compiler then
 // waits only for the loads into that stage, not for the group in flight
 // into the other one.
-constexpr int kFRT = 9;   // row tiles kept in registers
+constexpr int kFRT = 9;   // at most this many 16-row tiles
 constexpr int kFKG = 32;  // keys per group: two 16-key tiles
 
 template <int D>
@@ -493,35 +545,23 @@ struct KeyStage {
     static constexpr int RPI = 64 / CPR;         // key rows per load instruction
     static constexpr int NI = kFKG / RPI;        // load instructions per group
     static constexpr int ELEMS = kFKG * D;       // bf16 elements per group
-    static constexpr int ROW_LD = D + 8;         // row stride of the observation rows
-    static constexpr int ROW_ELEMS = kFRT * 16 * ROW_LD;
     // chunk position of logical chunk c of row r is c ^ swz(r)
     __device__ static int swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 };
 
 template <int D>
-struct alignas(16) StageA {
+struct alignas(16) StageBuf {
     uint16_t k[kWaves][KeyStage<D>::ELEMS];
 };
-template <int D>
-struct alignas(16) StageB {  // the observation rows are built here first
-    static constexpr int KE = kWaves * KeyStage<D>::ELEMS, RE = KeyStage<D>::ROW_ELEMS;
-    uint16_t e[KE > RE ? KE : RE];
-    __device__ uint16_t* k(int wave) { return e + wave * KeyStage<D>::ELEMS; }
-};
 
-template <int D>
 struct alignas(16) FastSmem {
     union {
         struct {
             float m[kWaves][kFRT * 16];
             float z[kWaves][kFRT * 16];
-        } red;                          // S items: per-wave row statistics
-        float best[kWaves * 256];       // F items: per-key maxima of the chunk
+        } red;                  // S items: per-wave row statistics
+        float nlse[kFRT * 16];  // F items: -lse of each row (raw-dot units)
     } v;
-    float nlse[kFRT * 16];
-    int act[kMaxC];
-    int nact;
 };
 
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
@@ -531,22 +571,66 @@ __device__ __forceinline__ void wait_vmem() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Start loading keys [kb, kb + 32) of the head into a wave's stage.  Load
-// instruction j writes 1 KB contiguous at stage + 1 KB * j, lane l's 16
-// bytes at offset 16 l: key row r = j*RPI + l / CPR, swizzled position
-// l % CPR, which holds logical chunk (l % CPR) ^ swz(r).  Each group of CPR
-// lanes reads one whole key row.  Keys past N read key N - 1.
+// Rows of head h into the workspace: row tile rt, vector v, lane l holds the
+// 16 bytes lane l presents to the MFMA, i.e. chunk 4 v + l / 16 of row
+// 16 rt + l % 16; plus the head's occupied-slot list.
+template <int D>
+__global__ __launch_bounds__(kThreads) void rows_kernel(Args a) {
+    constexpr int LD = D + 8, NV = Op<uint16_t, D>::NV;
+    __shared__ uint16_t y[kFRT * 16 * LD];
+    __shared__ int act[kMaxC];
+    __shared__ int nact;
+    const int h = blockIdx.x, tid = threadIdx.x;
+    active_slots(a, h, act, &nact);
+    build_rows<uint16_t, D, LD>(a, h, 0, a.R_pad_max, act, nact, y);
+    __syncthreads();
+    dev::u32x4* out = reinterpret_cast<dev::u32x4*>(a.rows) + (size_t)h * a.R_pad_max * D / 8;
+    const int n = a.R_pad_max / 16 * NV * 64;
+    for (int i = tid; i < n; i += kThreads) {
+        const int lane = i & 63, v = (i >> 6) % NV, rt = (i >> 6) / NV;
+        out[i] = *reinterpret_cast<const dev::u32x4*>(y + (rt * 16 + (lane & 15)) * LD + (4 * v + (lane >> 4)) * 8);
+    }
+    int* meta = a.rmeta + (size_t)h * kMetaWords;
+    if (tid == 0) meta[0] = nact;
+    for (int c = tid; c < nact; c += kThreads) meta[kMetaAct + c] = act[c];
+}
+
+template <int D, int RT>
+__device__ __forceinline__ void load_rows(const Args& a, int h, Op<uint16_t, D>* yr, int lane) {
+    constexpr int NV = Op<uint16_t, D>::NV;
+    const dev::u32x4* src = reinterpret_cast<const dev::u32x4*>(a.rows) + (size_t)h * RT * 16 * D / 8 + lane;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int v = 0; v < NV; ++v) yr[rt].v[v] = src[(rt * NV + v) * 64];
+}
+
+// Byte offset, within a group, of what lane `lane` loads with instruction
+// j: load instruction j writes 1 KB contiguous at stage + 1 KB * j, lane
+// l's 16 bytes at offset 16 l, which is key row r = j*RPI + l / CPR at
+// swizzled position l % CPR, holding logical chunk (l % CPR) ^ swz(r).
+// Each group of CPR lanes reads one whole key row.
+template <int D>
+__device__ __forceinline__ int group_offset(int j, int lane) {
+    using KS = KeyStage<D>;
+    const int r = j * KS::RPI + lane / KS::CPR;
+    return r * D * 2 + (((lane % KS::CPR) ^ KS::swz(r)) * 16);
+}
+
+// Start loading keys [kb, kb + 32) of the head into a wave's stage.  The
+// buffer resource covers keys [kb, min(N, kb + 32)) only, so rows past N
+// read as zero.
 template <int D>
 __device__ __forceinline__ void issue_group(const uint16_t* Kh, int kb, int N, uint16_t* stage, int lane) {
+#if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist in device code only
     using KS = KeyStage<D>;
-    const int rs = lane / KS::CPR, cs = lane % KS::CPR;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(Kh + (size_t)kb * D), (short)0, min(N - kb, kFKG) * D * 2, 0x00020000);
 #pragma unroll
-    for (int j = 0; j < KS::NI; ++j) {
-        const int r = j * KS::RPI + rs;
-        const uint16_t* src = Kh + (size_t)min(kb + r, N - 1) * D + ((cs ^ KS::swz(r)) * 8);
-        __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(stage + j * 512), 16, 0,
-                                         0);
-    }
+    for (int j = 0; j < KS::NI; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + j * 512),
+                                                 16, group_offset<D>(j, lane), 0, 0, 0);
+#endif
 }
 
 // MFMA operand of staged key tile t for lane (c16, g): vector v holds
@@ -561,86 +645,71 @@ __device__ __forceinline__ void read_key_tile(Op<uint16_t, D>& op, const uint16_
         op.v[v] = *reinterpret_cast<const dev::u32x4*>(row + ((4 * v + g) ^ KS::swz(r)) * 8);
 }
 
-// Build this head's rows in LDS (in stage B, which holds no keys yet) and
-// copy them into registers; every wave holds all of them.  Afterwards
-// stage B may be overwritten.
-template <int D>
-__device__ __forceinline__ int rows_to_registers(const Args& a, int h, FastSmem<D>& sm, StageB<D>& sb,
-                                                 Op<uint16_t, D>* yr, int c16, int g) {
-    constexpr int LD = KeyStage<D>::ROW_LD;
-    active_slots(a, h, sm.act, &sm.nact);
-    const int R = sm.nact + a.G * a.W, Rp = (R + 15) & ~15;
-    build_rows<uint16_t, D, LD>(a, h, 0, Rp, sm.act, sm.nact, sb.e);
-    __syncthreads();
-#pragma unroll
-    for (int rt = 0; rt < kFRT; ++rt)
-        if (rt < Rp / 16) load_row_tile<uint16_t, D>(yr[rt], sb.e + (rt * 16 + c16) * LD, g);
-    __syncthreads();  // every wave holds its rows: stage B may now take keys
-    return Rp / 16;
-}
-
 // Running (max, sum) of one S item over one staged group of 32 keys.
-template <int D>
-__device__ __forceinline__ void stats_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr, int RT,
-                                            float s2, float* m, float* z, int c16, int g) {
+// Keys at or past N (only in a head's last group, TAIL) enter with the
+// accumulator seeded at -inf, so they add exp2(-inf) = 0.
+template <int D, int RT, bool TAIL>
+__device__ __forceinline__ void stats_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr, float s2,
+                                            float* m, float* z, int c16, int g) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
-    f32x4 seed[2];  // 0 for keys below N, -inf past it
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int rt = 0; rt < RT; ++rt) {
+        f32x4 acc[2];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) seed[t][v] = (kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
+        for (int t = 0; t < 2; ++t) {
 #pragma unroll
-    for (int rt = 0; rt < kFRT; ++rt) {
-        if (rt < RT) {
-            f32x4 acc[2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                acc[t] = seed[t];
-                mma(acc[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
-            }
-            const float gm = fmaxf(fmaxf(fmaxf(acc[0][0], acc[0][1]), fmaxf(acc[0][2], acc[0][3])),
-                                   fmaxf(fmaxf(acc[1][0], acc[1][1]), fmaxf(acc[1][2], acc[1][3])));
-            const float mnew = fmaxf(m[rt], gm * s2);
-            const float ms = (mnew == -INFINITY) ? 0.f : mnew;  // no valid key yet: sums stay 0
-            float zz = z[rt] * fast_exp2(m[rt] - ms);
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(acc[t][v], s2, -ms));
-            z[rt] = zz;
-            m[rt] = mnew;
+            for (int v = 0; v < 4; ++v) acc[t][v] = (!TAIL || kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
+            mma(acc[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
         }
+        const float gm = fmaxf(fmaxf(fmaxf(acc[0][0], acc[0][1]), fmaxf(acc[0][2], acc[0][3])),
+                               fmaxf(fmaxf(acc[1][0], acc[1][1]), fmaxf(acc[1][2], acc[1][3])));
+        const float mnew = fmaxf(m[rt], gm * s2);
+        const float ms = (mnew == -INFINITY) ? 0.f : mnew;  // no valid key yet: sums stay 0
+        float zz = z[rt] * fast_exp2(m[rt] - ms);
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(acc[t][v], s2, -ms));
+        z[rt] = zz;
+        m[rt] = mnew;
+        // one row tile at a time: hoisting later tiles' MFMAs would keep
+        // their accumulators live and spill the registers that hold the rows
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
-// Per-key maxima of one F item over one staged group of 32 keys.
-template <int D>
-__device__ __forceinline__ void final_group(const uint16_t* st, int kofs, const Op<uint16_t, D>* yr, int RT,
-                                            const float* nlse, float* best_out, int c16, int g) {
+// Scores of one F item's staged group of 32 keys: per key the maximum over
+// rows, written straight out (64 contiguous bytes per 16-key tile).
+template <int D, int RT>
+__device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr,
+                                            const float* nlse, float* out, float s2ln2, int c16, int g) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
     float best[2] = {-INFINITY, -INFINITY};
 #pragma unroll
-    for (int rt = 0; rt < kFRT; ++rt) {
-        if (rt < RT) {
-            const f32x4 c0 = *reinterpret_cast<const f32x4*>(nlse + rt * 16 + 4 * g);
+    for (int rt = 0; rt < RT; ++rt) {
+        // re-read every group: hoisted out of the key loop these would hold
+        // 4 * RT more registers for the whole item
+        int off = rt * 16 + 4 * g;
+        asm volatile("" : "+v"(off));
+        const f32x4 c0 = *reinterpret_cast<const f32x4*>(nlse + off);
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                f32x4 acc = c0;
-                mma(acc, yr[rt], kop[t]);  // rows = observation rows, columns = keys
-                best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
-            }
+        for (int t = 0; t < 2; ++t) {
+            f32x4 acc = c0;
+            mma(acc, yr[rt], kop[t]);  // rows = observation rows, columns = keys
+            best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
         }
+        __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
         float b = best[t];
         b = fmaxf(b, dev::shfl_xor_f(b, 16));
         b = fmaxf(b, dev::shfl_xor_f(b, 32));
-        if (g == t) best_out[kofs + t * 16 + c16] = b;
+        if (g == t && kb + t * 16 + c16 < N) out[kb + t * 16 + c16] = b * s2ln2;
     }
 }
 
@@ -654,10 +723,10 @@ __device__ __forceinline__ void wait_group(bool more) {
         wait_vmem<0>();
 }
 
-template <int D, int GPW>
-__device__ void fast_stats(const Args& a, int h, int chunk, FastSmem<D>& sm, StageA<D>& sa, StageB<D>& sb,
-                           int* s_flag) {
-    constexpr int KPW = GPW * kFKG, KC = kWaves * KPW;
+template <int D, int RT>
+__device__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
+                           const Op<uint16_t, D>* yr, int* s_flag) {
+    const int KC = a.key_chunk, KPW = KC / kWaves, GPW = KPW / kFKG;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
@@ -666,15 +735,13 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem<D>& sm, Sta
     const int kw = chunk * KC + wave * KPW;
     const int ngroups = max(0, min(GPW, (N - kw + kFKG - 1) / kFKG));
     uint16_t* stA = sa.k[wave];
-    uint16_t* stB = sb.k(wave);
-    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);  // in flight while the rows are built
-    Op<uint16_t, D> yr[kFRT];
-    const int RT = rows_to_registers<D>(a, h, sm, sb, yr, c16, g);
+    uint16_t* stB = sb.k[wave];
+    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
     if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
     const float s2 = a.s2;
-    float m[kFRT], z[kFRT];
+    float m[RT], z[RT];
 #pragma unroll
-    for (int i = 0; i < kFRT; ++i) {
+    for (int i = 0; i < RT; ++i) {
         m[i] = -INFINITY;
         z[i] = 0.f;
     }
@@ -682,24 +749,28 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem<D>& sm, Sta
     for (int kg = 0; kg < ngroups; kg += 2) {
         const int kb = kw + kg * kFKG;
         wait_group<D>(kg + 1 < ngroups);
-        stats_group<D>(stA, kb, N, yr, RT, s2, m, z, c16, g);
+        if (kb + kFKG <= N)
+            stats_group<D, RT, false>(stA, kb, N, yr, s2, m, z, c16, g);
+        else
+            stats_group<D, RT, true>(stA, kb, N, yr, s2, m, z, c16, g);
         if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
         if (kg + 1 < ngroups) {
             wait_group<D>(kg + 2 < ngroups);
-            stats_group<D>(stB, kb + kFKG, N, yr, RT, s2, m, z, c16, g);
+            if (kb + 2 * kFKG <= N)
+                stats_group<D, RT, false>(stB, kb + kFKG, N, yr, s2, m, z, c16, g);
+            else
+                stats_group<D, RT, true>(stB, kb + kFKG, N, yr, s2, m, z, c16, g);
             if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
         }
     }
     // lanes sharing a row: g = 0..3, then waves
 #pragma unroll
-    for (int rt = 0; rt < kFRT; ++rt) {
-        if (rt < RT) {
-            merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 16), dev::shfl_xor_f(z[rt], 16));
-            merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 32), dev::shfl_xor_f(z[rt], 32));
-            if (g == 0) {
-                sm.v.red.m[wave][rt * 16 + c16] = m[rt];
-                sm.v.red.z[wave][rt * 16 + c16] = z[rt];
-            }
+    for (int rt = 0; rt < RT; ++rt) {
+        merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 16), dev::shfl_xor_f(z[rt], 16));
+        merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 32), dev::shfl_xor_f(z[rt], 32));
+        if (g == 0) {
+            sm.v.red.m[wave][rt * 16 + c16] = m[rt];
+            sm.v.red.z[wave][rt * 16 + c16] = z[rt];
         }
     }
     __syncthreads();
@@ -711,122 +782,98 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem<D>& sm, Sta
         dev::st_coherent(a.part_m + pbase + r, mm);
         dev::st_coherent(a.part_z + pbase + r, zz);
     }
-    publish_stats(a, h, sm.act, sm.nact, s_flag);
+    if (count_stats(a, h, s_flag)) {
+        const int* meta = a.rmeta + (size_t)h * kMetaWords;
+        fold_and_publish(a, h, meta + kMetaAct, meta[0], a.hctl + (size_t)h * kHcWords);
+    }
 }
 
-template <int D, int GPW>
-__device__ void fast_final(const Args& a, int h, int chunk, FastSmem<D>& sm, StageA<D>& sa, StageB<D>& sb,
-                           int* s_flag) {
-    constexpr int KPW = GPW * kFKG, KC = kWaves * KPW;
+template <int D, int RT>
+__device__ void fast_final(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
+                           const Op<uint16_t, D>* yr, int* s_flag) {
+    const int KC = a.key_chunk, KPW = KC / kWaves, GPW = KPW / kFKG;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
     const uint16_t* Kh = reinterpret_cast<const uint16_t*>(a.K) + (size_t)h * a.N_cap * D;
     const int N = a.N;
-    const int k0 = chunk * KC, kw = k0 + wave * KPW;
+    const int kw = chunk * KC + wave * KPW;
     const int ngroups = max(0, min(GPW, (N - kw + kFKG - 1) / kFKG));
     uint16_t* stA = sa.k[wave];
-    uint16_t* stB = sb.k(wave);
-    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);  // in flight while lse is awaited
+    uint16_t* stB = sb.k[wave];
+    // both stages in flight while lse is awaited
+    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
+    if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
     if (!await_lse(a, h, s_flag)) {
         wait_vmem<0>();  // no load may land in LDS after this workgroup ends
         return;
     }
-    Op<uint16_t, D> yr[kFRT];
     const float inv_s2 = 1.0f / a.s2;
-    for (int r = tid; r < kFRT * 16; r += kThreads)
-        sm.nlse[r] = (r < a.R_pad_max) ? -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r) * inv_s2
-                                        : -INFINITY;
-    const int RT = rows_to_registers<D>(a, h, sm, sb, yr, c16, g);
-    if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
-    const int kofs = wave * KPW;  // this wave's keys within the chunk
-#pragma unroll 1
-    for (int kg = 0; kg < ngroups; kg += 2) {
-        wait_group<D>(kg + 1 < ngroups);
-        final_group<D>(stA, kofs + kg * kFKG, yr, RT, sm.nlse, sm.v.best, c16, g);
-        if (kg + 2 < ngroups) issue_group<D>(Kh, kw + (kg + 2) * kFKG, N, stA, lane);
-        if (kg + 1 < ngroups) {
-            wait_group<D>(kg + 2 < ngroups);
-            final_group<D>(stB, kofs + (kg + 1) * kFKG, yr, RT, sm.nlse, sm.v.best, c16, g);
-            if (kg + 3 < ngroups) issue_group<D>(Kh, kw + (kg + 3) * kFKG, N, stB, lane);
-        }
-    }
+    for (int r = tid; r < RT * 16; r += kThreads)
+        sm.v.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r) * inv_s2;
     __syncthreads();
     float* out = a.scores + (size_t)h * N;
-    for (int i = tid; i < KC; i += kThreads)
-        if (k0 + i < N) out[k0 + i] = sm.v.best[i] * a.s2ln2;
+    const float s2ln2 = a.s2ln2;
+#pragma unroll 1
+    for (int kg = 0; kg < ngroups; kg += 2) {
+        const int kb = kw + kg * kFKG;
+        wait_group<D>(kg + 1 < ngroups);
+        final_group<D, RT>(stA, kb, N, yr, sm.v.nlse, out, s2ln2, c16, g);
+        if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
+        if (kg + 1 < ngroups) {
+            wait_group<D>(kg + 2 < ngroups);
+            final_group<D, RT>(stB, kb + kFKG, N, yr, sm.v.nlse, out, s2ln2, c16, g);
+            if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
+        }
+    }
 }
 
-// ---- kernel entry, shared by both paths ------------------------------------
-struct NoStage {
-    int unused;
-};
-template <typename T, int D, int KGN>
-struct GenericPath {
-    using Shared = Smem<T, D>;
-    using SA = NoStage;
-    using SB = NoStage;
-    __device__ static void stats(const Args& a, int h, int c, Shared& sm, SA&, SB&, int* f) {
-        stats_item<T, D, KGN>(a, h, c, sm, f);
-    }
-    __device__ static void final(const Args& a, int h, int c, Shared& sm, SA&, SB&, int* f) {
-        final_item<T, D, KGN>(a, h, c, sm, f);
-    }
-};
-template <int D, int GPW>
-struct FastPath {
-    using Shared = FastSmem<D>;
-    using SA = StageA<D>;
-    using SB = StageB<D>;
-    __device__ static void stats(const Args& a, int h, int c, Shared& sm, SA& sa, SB& sb, int* f) {
-        fast_stats<D, GPW>(a, h, c, sm, sa, sb, f);
-    }
-    __device__ static void final(const Args& a, int h, int c, Shared& sm, SA& sa, SB& sb, int* f) {
-        fast_final<D, GPW>(a, h, c, sm, sa, sb, f);
-    }
-};
-
-template <class Path>
-__global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
-    __shared__ typename Path::Shared sm;
-    __shared__ typename Path::SA sa;
-    __shared__ typename Path::SB sb;
+template <int D, int RT>
+__global__ __launch_bounds__(kThreads, 2) void fast_score_kernel(Args a) {
+    __shared__ FastSmem sm;
+    __shared__ StageBuf<D> sa;
+    __shared__ StageBuf<D> sb;
     __shared__ int s_ticket, s_ok, s_flag;
-    const int tid = threadIdx.x;
     const int h = head_of_block(a, blockIdx.x);
-    int* hc = a.hctl + (size_t)h * kHcWords;
-    if (tid == 0) {
-        s_ok = dev::stamp_ok(a.hdr, a.P, a.budget);
-        if (s_ok)
-            s_ticket = dev::fetch_add_relaxed(hc + kHcScTicket, 1);
-        else
-            dev::raise_error(a.hdr, kErrStamp);
-    }
-    __syncthreads();
-    if (!s_ok) return;
-    if (s_ticket >= 2 * a.nch) {  // control block was not clear: do nothing
-        if (tid == 0) dev::raise_error(a.hdr, kErrStamp);
+    Op<uint16_t, D> yr[RT];
+    load_rows<D, RT>(a, h, yr, threadIdx.x & 63);  // in flight with the ticket
+    if (!take_ticket(a, h, &s_ticket, &s_ok)) {
+        wait_vmem<0>();
         return;
     }
-    if (s_ticket < a.nch)
-        Path::stats(a, h, s_ticket, sm, sa, sb, &s_flag);
+    const int ticket = __builtin_amdgcn_readfirstlane(s_ticket);
+    if (ticket < a.nch)
+        fast_stats<D, RT>(a, h, ticket, sm, sa, sb, yr, &s_flag);
     else
-        Path::final(a, h, s_ticket - a.nch, sm, sa, sb, &s_flag);
-    // The head's last workgroup to finish clears its control words.
-    __syncthreads();
-    if (tid == 0) s_flag = (dev::fetch_add_relaxed(hc + kHcScDone, 1) == 2 * a.nch - 1);
-    __syncthreads();
-    if (s_flag && tid == 0) {
-        dev::st_flag(hc + kHcScTicket, 0);
-        dev::st_flag(hc + kHcScDone, 0);
-        dev::st_flag(hc + kHcP1Count, 0);
-        dev::st_flag(hc + kHcReady, 0);
+        fast_final<D, RT>(a, h, ticket - a.nch, sm, sa, sb, yr, &s_flag);
+    finish_item(a, h, &s_flag);
+}
+
+template <int D, int RT>
+hipError_t launch_fast_rt(const Args& a, hipStream_t s) {
+    hipLaunchKernelGGL((rows_kernel<D>), dim3(a.P), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((fast_score_kernel<D, RT>), dim3(a.total), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_fast(const Args& a, hipStream_t s) {
+    switch (a.R_pad_max / 16) {
+        case 1: return launch_fast_rt<D, 1>(a, s);
+        case 2: return launch_fast_rt<D, 2>(a, s);
+        case 3: return launch_fast_rt<D, 3>(a, s);
+        case 4: return launch_fast_rt<D, 4>(a, s);
+        case 5: return launch_fast_rt<D, 5>(a, s);
+        case 6: return launch_fast_rt<D, 6>(a, s);
+        case 7: return launch_fast_rt<D, 7>(a, s);
+        case 8: return launch_fast_rt<D, 8>(a, s);
+        default: return launch_fast_rt<D, 9>(a, s);
     }
 }
 
-template <class Path>
+template <typename T, int D, int KGN>
 hipError_t launch_t(const Args& a, hipStream_t s) {
-    hipLaunchKernelGGL((score_kernel<Path>), dim3(a.total), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((score_kernel<T, D, KGN>), dim3(a.total), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
@@ -863,6 +910,7 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
     a.budget = d.budget;
     a.R_pad_max = L.R_pad_max;
     a.nch = L.nch;
+    a.key_chunk = L.key_chunk;
     // Lag between a head's S and F items: about one machine-full of items.
     int dev_id = 0, cus = 256;
     if (hipGetDevice(&dev_id) != hipSuccess ||
@@ -875,15 +923,16 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
     a.s2 = sc * 1.4426950408889634f;
     a.s2ln2 = a.s2 * 0.69314718055994531f;
     const bool bf = d.dtype == BKV_BF16;
-    const bool k4 = L.kgn == 4;  // 1024-key items (else 256)
     if (bf && L.R_pad_max <= kFRT * 16) {  // all rows fit in registers
-        if (d.D == 128) return k4 ? launch_t<FastPath<128, 8>>(a, s) : launch_t<FastPath<128, 2>>(a, s);
-        return k4 ? launch_t<FastPath<64, 8>>(a, s) : launch_t<FastPath<64, 2>>(a, s);
+        a.rows = reinterpret_cast<uint16_t*>(w + L.rows);
+        a.rmeta = reinterpret_cast<int*>(w + L.rmeta);
+        return d.D == 128 ? launch_fast<128>(a, s) : launch_fast<64>(a, s);
     }
-    if (bf && d.D == 128) return k4 ? launch_t<GenericPath<uint16_t, 128, 4>>(a, s) : launch_t<GenericPath<uint16_t, 128, 1>>(a, s);
-    if (bf) return k4 ? launch_t<GenericPath<uint16_t, 64, 4>>(a, s) : launch_t<GenericPath<uint16_t, 64, 1>>(a, s);
-    if (d.D == 128) return k4 ? launch_t<GenericPath<float, 128, 4>>(a, s) : launch_t<GenericPath<float, 128, 1>>(a, s);
-    return k4 ? launch_t<GenericPath<float, 64, 4>>(a, s) : launch_t<GenericPath<float, 64, 1>>(a, s);
+    const bool k4 = L.kgn == 4;  // 1024-key items (else 256)
+    if (bf && d.D == 128) return k4 ? launch_t<uint16_t, 128, 4>(a, s) : launch_t<uint16_t, 128, 1>(a, s);
+    if (bf) return k4 ? launch_t<uint16_t, 64, 4>(a, s) : launch_t<uint16_t, 64, 1>(a, s);
+    if (d.D == 128) return k4 ? launch_t<float, 128, 4>(a, s) : launch_t<float, 128, 1>(a, s);
+    return k4 ? launch_t<float, 64, 4>(a, s) : launch_t<float, 64, 1>(a, s);
 }
 
 }  // namespace bkv
