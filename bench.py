@@ -33,6 +33,39 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 
 METRIC = "cached tokens scored+compacted/s per layer; eviction latency µs (Qwen3-4B, 32K)"
 
+# Measured HBM traffic of the score kernels on this workload (rocprofv3 FETCH_SIZE and
+# WRITE_SIZE, calibrated); used only while the kernel sources are unchanged since.
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "score_qwen3-4b-32k.md")
+SCORE_SOURCES = ("paper_2609_04971_amd/csrc/score.hip", "paper_2609_04971_amd/csrc/device_common.h",
+                 "paper_2609_04971_amd/csrc/internal.h", "include/bkv.h", "paper_2609_04971_amd/build.py")
+
+
+def score_source_digest() -> str:
+    """sha256 over the files the score kernels are built from."""
+    import hashlib
+    h = hashlib.sha256()
+    for rel in SCORE_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """Bytes per score launch from the committed profile, or None when the
+    profile is missing or was taken on different kernel sources."""
+    try:
+        with open(TRAFFIC_PROFILE) as f:
+            fields = dict(line.split(":", 1) for line in f.read().splitlines() if line.startswith(("source_sha256:",
+                                                                                                  "traffic_bytes_per_launch:")))
+    except OSError:
+        return None
+    if fields.get("source_sha256", "").strip() != score_source_digest():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"].strip())
+    except (KeyError, ValueError):
+        return None
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -41,7 +74,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layers", type=int, default=None, help="layers resident (default: the workload's 36)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-heads", type=int, default=512,
+    ap.add_argument("--cpu-heads", type=int, default=768,
                     help="(batch, kv-head) pairs in the CPU oracle sample, taken layer by layer")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
@@ -138,8 +171,8 @@ def main():
     score_s = avg_us["score"] * 1e-6
     achieved = score_bytes / score_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": "score_kernel<bf16,128,1024-key items>",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+                "kernel": "score launch: rows_kernel<128> + fast_score_kernel<128, 9>",
                 "algorithmic_bytes": score_bytes,
                 "mfma_tflops": round(score_flops / score_s / 1e12, 1),
                 "mfma_frac": round(score_flops / score_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}

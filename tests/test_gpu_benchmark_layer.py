@@ -1,0 +1,67 @@
+"""GPU parity at the benchmark's full size: whole Qwen3-4B-shaped layers at
+32K tokens (B=16, Hkv=8, D=128, N=32768, R=144, budget 4096), evicted by the
+same calls bench.py times (score -> top-k -> compact on one workspace).
+Sampled heads are checked against the oracle, which computes them one by one;
+properties that hold at any size are checked on every head."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import assert_rows_match, assert_scores_close, compare_kept, dims_of, host, say
+import paper_2609_04971_amd as bkv
+from paper_2609_04971_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+BATCHES = [0, 7, 15]                           # batches copied to the host
+HEADS = [(0, 0), (0, 7), (1, 3), (2, 0), (2, 7)]  # (index into BATCHES, kv-head)
+
+
+def _host_batches(x):
+    per_batch = ("K", "V", "q_win", "beacons", "counts")
+    return {k: host(v[BATCHES]) if k in per_batch else host(v) for k, v in x.items()}
+
+
+def test_benchmark_layers_sampled_heads():
+    w = synth.QWEN3_4B_32K
+    d = dims_of(w)
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    scores = torch.empty(d.B, d.Hkv, d.N, device="cuda")
+    kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
+    for layer in (0, 1):  # the second layer reuses the workspace, as the benchmark does
+        x = synth.make_layer(w, seed=100 + layer, device="cuda")
+        xh = _host_batches(x)
+        say(f"benchmark layer {layer}: {d}")
+        bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+                  rope_sin=x["rope_sin"])
+        bkv.topk(d, scores, kept)
+        bkv.compact(d, x["K"], x["V"], kept, ws)
+        torch.cuda.synchronize()
+        assert bkv.device_status(ws) == bkv.OK
+
+        # every head: scores are log-probabilities, kept is ascending and
+        # holds the recent window
+        s_all = host(scores).numpy()
+        k_all = host(kept).numpy()
+        assert not np.isnan(s_all).any() and np.all(s_all <= 1e-4)
+        assert np.all(np.diff(k_all, axis=-1) > 0)
+        assert np.array_equal(k_all[..., -w.W:], np.broadcast_to(np.arange(w.N - w.W, w.N), k_all[..., -w.W:].shape))
+
+        say(f"benchmark layer {layer}: oracle on {len(HEADS)} heads")
+        ref = oracle.evict(xh["K"], xh["V"], xh["q_win"], xh["beacons"], xh["counts"], N=w.N, budget=w.budget,
+                           W=w.W, rope_cos=xh["rope_cos"], rope_sin=xh["rope_sin"], heads=HEADS,
+                           threads=len(HEADS))
+        bi = np.array([BATCHES[b] for b, _ in HEADS])
+        hi = np.array([h for _, h in HEADS])
+        li = np.array([b for b, _ in HEADS])
+        assert_scores_close(s_all[bi, hi], ref["scores"][li, hi])
+        kg, kr = k_all[bi, hi], ref["kept"][li, hi]
+        band, diff = compare_kept(kg, kr, ref["scores"][li, hi], w.N, w.W, 0, w.budget)
+        say(f"benchmark layer {layer}: tie band {band}, {diff} in-band differences")
+        K_gpu = host(x["K"][torch.as_tensor(bi), torch.as_tensor(hi)])
+        V_gpu = host(x["V"][torch.as_tensor(bi), torch.as_tensor(hi)])
+        assert_rows_match(K_gpu, ref["K"][li, hi], kg, kr, d.n_keep, "K")
+        assert_rows_match(V_gpu, ref["V"][li, hi], kg, kr, d.n_keep, "V")
+        del x
+        torch.cuda.empty_cache()
