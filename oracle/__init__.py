@@ -56,6 +56,8 @@ def _load():
     lib.orc_topk.restype = _i
     lib.orc_compact.argtypes = [_i, _i, _i, _p, _p, _p]
     lib.orc_compact.restype = _i
+    lib.orc_fps.argtypes = [_i, _i, _i, _i, _p, _p, ctypes.c_double, _p, _p]
+    lib.orc_fps.restype = _i
     lib.orc_evict_head.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p,
                                    _p, _f, _p, _p, _p]
     lib.orc_evict_head.restype = _i
@@ -290,3 +292,31 @@ def evict(K, V, q_win, beacons, counts, N: int, budget: int, W: int, n_prefix: i
 
     _run(one, list(heads), threads)
     return {"K": k, "V": v, "scores": scores, "row_lse": lse, "kept": kept}
+
+
+def fps(q, m: int, forced=None, tie_tol: float = 0.0, threads: int = 1):
+    """Farthest point sampling (Appendix D.1, Algorithm 1) of every head of
+    q [H, n, D] (bf16 or fp32): returns (picks [H, min(m, n)] int32 in
+    selection order, near_tie [H, min(m, n)] bool).  With `forced`
+    [H, min(m, n)], each forced pick is checked to be within tie_tol of the
+    step's minimum and then followed (ValueError at the first that is not)."""
+    lib = _load()
+    x, dt = _raw(q)
+    H, n, D = x.shape
+    k = max(0, min(m, n))
+    picks = np.zeros((H, k), np.int32)
+    tie = np.zeros((H, k), np.int32)
+    fo = None if forced is None else np.ascontiguousarray(np.asarray(forced), dtype=np.int32)
+    errors = {}
+
+    def one(h):
+        rc = lib.orc_fps(dt, D, n, m, _ptr(x, h * n * D), None if fo is None else _ptr(fo, h * k), float(tie_tol),
+                         _ptr(picks, h * k) if k else None, _ptr(tie, h * k) if k else None)
+        if rc < 0:
+            errors[h] = -rc - 1
+
+    _run(one, list(range(H)), threads)
+    if errors:
+        h = min(errors)
+        raise ValueError(f"head {h}: forced pick at step {errors[h]} is not within {tie_tol} of the minimum")
+    return picks, tie.astype(bool)

@@ -375,3 +375,89 @@ int orc_evict_head(int dtype, int D, int N, int C, int G, int W, int budget, int
     rc = orc_compact(dtype == ORC_BF16 ? 2 : 4, D, n, kept, Khead, Vhead);
     return rc ? rc : n;
 }
+
+/* ---- farthest point sampling over pre-RoPE queries ----------------------
+ *
+ * Appendix D.1 (Algorithm 1), the selection step of Continual FPS
+ * (Section 4.2; Algorithm 2 calls it as FPS(Q, B_Q^min)).  From n queries
+ * of dimension D pick min(m, n) of them, in selection order:
+ *
+ *   avg_i = (1/n) sum_j cos(q_i, q_j)     (j = i included)
+ *   p     = argmin_i avg_i                (first pick)
+ *   S_j   = cos(q_j, q_p)
+ *   then repeatedly r = argmin over unpicked j of S_j, pick r, and
+ *   S_j <- max(S_j, cos(q_j, q_r)) for the unpicked j.
+ *
+ * cos(x, y) = x.y / (|x| |y|), taken as 0 when either norm is 0.  Ties go
+ * to the lowest index.  The cosines are computed here pairwise, straight
+ * from the definition (O(n^2 D)).
+ *
+ * forced (optional): a selection to follow instead of the argmins, as long
+ * as each forced pick is within tie_tol of that step's minimum (else the
+ * function returns -(step + 1)); near_tie (optional) flags the steps whose
+ * minimum is shared, within tie_tol, by another candidate.  This lets a
+ * test check a selection made in another precision step by step.
+ * Returns the number of picks.
+ */
+static double orc_cos(const void* q, int dtype, int D, int i, int j) {
+    double dot = 0.0, ni = 0.0, nj = 0.0;
+    for (int d = 0; d < D; ++d) {
+        const double a = elem(q, (size_t)i * D + d, dtype), b = elem(q, (size_t)j * D + d, dtype);
+        dot += a * b;
+        ni += a * a;
+        nj += b * b;
+    }
+    if (ni == 0.0 || nj == 0.0) return 0.0;
+    return dot / (sqrt(ni) * sqrt(nj));
+}
+
+int orc_fps(int dtype, int D, int n, int m, const void* q, const int32_t* forced, double tie_tol,
+            int32_t* out, int32_t* near_tie) {
+    const int k_max = m < n ? m : n;
+    if (k_max <= 0) return 0;
+    double* val = (double*)malloc(sizeof(double) * (size_t)n);
+    unsigned char* picked = (unsigned char*)calloc((size_t)n, 1);
+    if (!val || !picked) {
+        free(val);
+        free(picked);
+        return -1000000;
+    }
+    /* average cosine of each query against all of them */
+    for (int i = 0; i < n; ++i) {
+        double s = 0.0;
+        for (int j = 0; j < n; ++j) s += orc_cos(q, dtype, D, i, j);
+        val[i] = s / (double)n;
+    }
+    int rc = k_max;
+    for (int k = 0; k < k_max; ++k) {
+        /* the step's minimum over unpicked candidates (val = avg for the
+           first pick, S afterwards), lowest index on ties */
+        int best = -1;
+        for (int j = 0; j < n; ++j)
+            if (!picked[j] && (best < 0 || val[j] < val[best])) best = j;
+        int tie = 0;
+        for (int j = 0; j < n; ++j)
+            if (!picked[j] && j != best && val[j] <= val[best] + tie_tol) tie = 1;
+        int r = best;
+        if (forced) {
+            r = forced[k];
+            if (r < 0 || r >= n || picked[r] || val[r] > val[best] + tie_tol) {
+                rc = -(k + 1);
+                break;
+            }
+        }
+        out[k] = r;
+        if (near_tie) near_tie[k] = tie;
+        picked[r] = 1;
+        /* nearest-picked similarity: S_j = cos(q_j, q_r) after the first
+           pick, then the running maximum */
+        for (int j = 0; j < n; ++j) {
+            if (picked[j]) continue;
+            const double c = orc_cos(q, dtype, D, j, r);
+            val[j] = (k == 0) ? c : (c > val[j] ? c : val[j]);
+        }
+    }
+    free(val);
+    free(picked);
+    return rc;
+}
