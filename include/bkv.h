@@ -169,6 +169,46 @@ bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, con
                      float scale, int32_t* kept, float* scores, float* row_lse, void* ws,
                      size_t ws_bytes, hipStream_t stream);
 
+/* ---- Continual FPS: the paper's own beacon selection ------------------------
+ * Farthest point sampling under cosine similarity (Appendix D.1, Algorithm 1)
+ * of H independent query sets ("heads"), each the first n rows of
+ * q [H, q_rows, D] (pre-RoPE queries, dtype BKV_BF16 or BKV_F32, row stride D,
+ * head stride q_rows*D elements, 16-byte aligned).  Per head, with cos = 0
+ * whenever either norm is 0:
+ *   avg_i = mean over all n rows j (j = i included) of cos(q_i, q_j);
+ *   the first pick is argmin_i avg_i; S_j = cos(q_j, first pick);
+ *   each further pick is r = argmin over unpicked j of S_j, after which
+ *   S_j <- max(S_j, cos(q_j, q_r)) for the unpicked j;
+ * every argmin takes the lowest index among equal values, and the picks are
+ * emitted in selection order, k = min(m, n) of them (m >= n returns every
+ * row).  Cosines are computed in fp32 (exact bf16 products, fp32 sums).
+ * Limits: D in {64, 128}; 0 <= n <= q_rows; n <= 32768; H, m >= 0
+ * (H, n or m of 0 enqueue nothing).  Needs no workspace. */
+
+/* picks [H, min(m, n)] int32 written: the selected row indices of each head. */
+bkv_status bkv_fps(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* q,
+                   int32_t q_rows, int32_t* picks, hipStream_t stream);
+
+/* FPS followed by the gather of the selection, which is the fill-and-compress
+ * step Q_obs <- FPS(Q_obs, B_Q^min) of Section 4.2 (Eq. fps_q) and also serves
+ * the prefill initialisation and the post-eviction re-selection of
+ * Algorithm 2: rows 0..k-1 of each head of dst [H, dst_rows, D] become the
+ * picked rows of src in selection order, k = min(m, n), converted to
+ * dst_dtype (BKV_F32 always; otherwise equal to dtype), bit for bit when
+ * the type is unchanged; rows k..dst_rows-1 are left as they were.
+ * dst may be src itself (then dst_dtype == dtype and dst_rows == src_rows:
+ * every picked row is read before any is written); any other overlap is
+ * BKV_ERR_INVALID.  picks [H, k] int32 is an optional output (NULL to skip).
+ * counts, optional [H, dst_rows] int32, is set to 1 for rows < k and 0 for
+ * the rest, so that for H = B*Hq and dst_rows = n_beacon, dst written as
+ * fp32 is directly the beacons [B, Hkv, G*n_beacon, D] and counts argument
+ * of bkv_score: the union of the query heads' beacon sets of each group
+ * (Algorithm 2, the group-level beacon set).  Limits: those of bkv_fps,
+ * plus k <= 128 and dst_rows >= k. */
+bkv_status bkv_fps_gather(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* src,
+                          int32_t src_rows, void* dst, int32_t dst_dtype, int32_t dst_rows, int32_t* picks,
+                          int32_t* counts, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* bkv_status_string(bkv_status s);
 

@@ -24,7 +24,7 @@ OP_BEACON_UPDATE, OP_SCORE, OP_TOPK, OP_COMPACT, OP_EVICT = range(5)
 
 EXPORTS = ("bkv_validate", "bkv_workspace_bytes", "bkv_workspace_init", "bkv_device_status",
            "bkv_beacon_update", "bkv_score", "bkv_topk", "bkv_compact", "bkv_evict",
-           "bkv_status_string", "bkv_abi_version")
+           "bkv_fps", "bkv_fps_gather", "bkv_status_string", "bkv_abi_version")
 
 
 class Dims(ctypes.Structure):
@@ -65,6 +65,7 @@ def dims(B, Hq, Hkv, D, N, W, C, budget, n_prefix=0, dtype="bf16", N_cap=None) -
 _P = ctypes.c_void_p
 _D = ctypes.POINTER(Dims)
 _S = ctypes.c_size_t
+_I = ctypes.c_int32
 _SIGS = {
     "bkv_validate": ([_D, ctypes.c_int32], ctypes.c_int),
     "bkv_workspace_bytes": ([_D, ctypes.c_int32], _S),
@@ -75,6 +76,8 @@ _SIGS = {
     "bkv_topk": ([_D, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_compact": ([_D, _P, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_evict": ([_D, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_fps": ([_I] * 5 + [_P, _I, _P, _P], ctypes.c_int),
+    "bkv_fps_gather": ([_I] * 5 + [_P, _I, _P, _I, _I, _P, _P, _P], ctypes.c_int),
     "bkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "bkv_abi_version": ([], ctypes.c_int32),
 }
@@ -242,3 +245,55 @@ def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row
         _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True), wp, wn,
         _stream())
     _check(st, "bkv_evict")
+
+
+# ---- Continual FPS -------------------------------------------------------------
+_FPS_DT = {torch.bfloat16: BF16, torch.float32: F32}
+
+
+def _fps_src(q, n, name):
+    if not isinstance(q, torch.Tensor) or q.dim() < 2:
+        raise ValueError(f"{name} must be a tensor [..., rows, D]")
+    if q.dtype not in _FPS_DT:
+        raise ValueError(f"{name} must be bfloat16 or float32, got {q.dtype}")
+    rows, D = q.shape[-2], q.shape[-1]
+    H = q.numel() // max(1, rows * D) if rows * D else 0
+    n = rows if n is None else int(n)
+    return _ptr(q, name=name), H, rows, D, n
+
+
+def fps(q, m: int, n: int | None = None, picks=None):
+    """Farthest point sampling (Appendix D.1, Algorithm 1) of the first n rows
+    (default: all) of every head of q [..., rows, D]: returns picks
+    [..., min(m, n)] int32 in selection order."""
+    qp, H, rows, D, n = _fps_src(q, n, "q")
+    k = max(0, min(int(m), n))
+    shape = tuple(q.shape[:-2]) + (k,)
+    if picks is None:
+        picks = torch.empty(shape, dtype=torch.int32, device=q.device)
+    pp = _ptr(picks, shape, torch.int32, "picks")
+    _check(lib().bkv_fps(H, n, int(m), D, _FPS_DT[q.dtype], qp, rows, pp, _stream()), "bkv_fps")
+    return picks
+
+
+def fps_gather(src, m: int, dst=None, n: int | None = None, picks=None, counts=None):
+    """FPS of the first n rows of every head of src [..., rows, D], then rows
+    0..k-1 of dst [..., dst_rows, D] (default: src itself, in place) become
+    the picked rows in selection order, k = min(m, n) (Section 4.2, Eq.
+    fps_q).  dst may be float32 for a bfloat16 src.  picks [..., k] and
+    counts [..., dst_rows] are optional outputs.  Returns dst."""
+    sp, H, rows, D, n = _fps_src(src, n, "src")
+    k = max(0, min(int(m), n))
+    if dst is None:
+        dst = src
+    if dst.dtype not in _FPS_DT or dst.dim() != src.dim() or dst.shape[:-2] != src.shape[:-2] \
+            or dst.shape[-1] != D:
+        raise ValueError("dst must be [..., dst_rows, D] with the leading shape and D of src")
+    dst_rows = dst.shape[-2]
+    lead = tuple(src.shape[:-2])
+    pp = _ptr(picks, lead + (k,), torch.int32, "picks", optional=True)
+    cp = _ptr(counts, lead + (dst_rows,), torch.int32, "counts", optional=True)
+    st = lib().bkv_fps_gather(H, n, int(m), D, _FPS_DT[src.dtype], sp, rows, _ptr(dst, name="dst"),
+                              _FPS_DT[dst.dtype], dst_rows, pp, cp, _stream())
+    _check(st, "bkv_fps_gather")
+    return dst

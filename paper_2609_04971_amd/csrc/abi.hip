@@ -17,6 +17,8 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 constexpr int kMaxRows = 1024;  // observation rows per head (C + G*W)
 constexpr int kMaxC = 64;
+constexpr int kFpsMaxN = 32768;     // rows per FPS head
+constexpr int kFpsMaxGather = 128;  // rows an FPS gather writes per head
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -221,6 +223,45 @@ bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, con
     e = launch_topk(*d, sc, kp, stream);
     if (e != hipSuccess) return BKV_ERR_HIP;
     return map_hip(launch_compact(*d, L, K, V, kp, ws, stream));
+}
+
+static bkv_status check_fps_args(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* q,
+                                 int32_t q_rows) {
+    if (dtype != BKV_F32 && dtype != BKV_BF16) return BKV_ERR_DTYPE;
+    if (D != 64 && D != 128) return BKV_ERR_SHAPE;
+    if (H < 0 || n < 0 || m < 0 || n > kFpsMaxN || q_rows < n) return BKV_ERR_SHAPE;
+    if ((long long)H * q_rows > 0x7fffffffLL) return BKV_ERR_SHAPE;
+    if (H > 0 && n > 0 && m > 0 && (!q || !aligned16(q))) return BKV_ERR_INVALID;
+    return BKV_OK;
+}
+
+bkv_status bkv_fps(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* q, int32_t q_rows,
+                   int32_t* picks, hipStream_t stream) {
+    bkv_status st = check_fps_args(H, n, m, D, dtype, q, q_rows);
+    if (st != BKV_OK) return st;
+    if (H == 0 || n == 0 || m == 0) return BKV_OK;
+    if (!picks) return BKV_ERR_INVALID;
+    const int k = m < n ? m : n;
+    return map_hip(launch_fps(H, n, k, D, dtype, q, q_rows, picks, nullptr, dtype, 0, nullptr, stream));
+}
+
+bkv_status bkv_fps_gather(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* src,
+                          int32_t src_rows, void* dst, int32_t dst_dtype, int32_t dst_rows, int32_t* picks,
+                          int32_t* counts, hipStream_t stream) {
+    bkv_status st = check_fps_args(H, n, m, D, dtype, src, src_rows);
+    if (st != BKV_OK) return st;
+    if (dst_dtype != BKV_F32 && dst_dtype != dtype) return BKV_ERR_DTYPE;
+    const int k = m < n ? m : n;
+    if (k > kFpsMaxGather || dst_rows < k || (long long)H * dst_rows > 0x7fffffffLL) return BKV_ERR_SHAPE;
+    if (H == 0 || n == 0 || m == 0) return BKV_OK;
+    if (!dst || !aligned16(dst)) return BKV_ERR_INVALID;
+    // dst is either src itself, with the same layout, or disjoint from it
+    const size_t src_bytes = (size_t)H * src_rows * D * (dtype == BKV_BF16 ? 2 : 4);
+    const size_t dst_bytes = (size_t)H * dst_rows * D * (dst_dtype == BKV_BF16 ? 2 : 4);
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+    const bool overlap = s0 < d0 + dst_bytes && d0 < s0 + src_bytes;
+    if (overlap && !(s0 == d0 && dst_dtype == dtype && dst_rows == src_rows)) return BKV_ERR_INVALID;
+    return map_hip(launch_fps(H, n, k, D, dtype, src, src_rows, picks, dst, dst_dtype, dst_rows, counts, stream));
 }
 
 const char* bkv_status_string(bkv_status s) {

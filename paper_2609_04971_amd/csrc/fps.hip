@@ -1,0 +1,485 @@
+// Continual FPS for gfx950: farthest point sampling of pre-RoPE queries
+// under cosine similarity (Appendix D.1, Algorithm 1), and the gather that
+// replaces a query buffer by its selection (Section 4.2, Eq. fps_q; the
+// FPS steps of Algorithm 2).
+//
+// One head per workgroup, two kernels by set size:
+//
+//  - fps_gram_kernel, n <= 64, one wave.  These are the buffers of the
+//    continual path (B_Q^max = n_beacon + n_recent rows).  The whole Gram
+//    matrix Q Q^T of the head comes from MFMA (exact bf16 products, fp32
+//    sums; fp32 input uses the fp32 MFMA), its diagonal gives the norms, and
+//    it is normalised to cosines in LDS once.  avg_i is then a column sum,
+//    and each pick costs one LDS read per lane and a wave argmin.
+//  - fps_stream_kernel, n up to 32768, 1024 threads.  Prefill-sized sets.
+//    Thread t owns rows j = t + 1024 i and keeps their S_j and 1/|q_j| in
+//    registers.  avg_i uses the regrouped sum
+//        sum_j cos(q_i, q_j) = (q_i / |q_i|) . sum_j (q_j / |q_j|),
+//    which is O(n D) instead of O(n^2 D); each pick re-reads every row once
+//    to form cos(q_j, q_r), so the kernel moves about (m + 3) n D elements.
+//
+// Both take the lowest index among equal values at every argmin, treat a
+// zero vector as having cosine 0 with everything, and emit the picks in
+// selection order.  The 1/n of avg_i is left out: it does not move the
+// argmin.
+#include <math.h>
+
+#include "device_common.h"
+#include "internal.h"
+
+namespace bkv {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+using dev::u32x4;
+
+constexpr int kGramMaxN = 64;
+constexpr int kLdg = kGramMaxN + 1;  // LDS row stride of the cosine matrix: mirrored writes hit distinct banks
+constexpr int kStreamThreads = 512;
+constexpr int kStreamWaves = kStreamThreads / 64;
+constexpr int kStreamMaxRpt = 64;  // rows per thread: n <= 32768
+constexpr int kMaxGather = 128;    // rows a gather may write per head
+
+// Elements per 16-byte chunk and their conversion to fp32.
+template <typename T>
+struct Elt;
+template <>
+struct Elt<uint16_t> {
+    static constexpr int EV = 8;
+    __device__ static void unpack(const u32x4& c, float* f) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            f[2 * i] = __uint_as_float(c[i] << 16);
+            f[2 * i + 1] = __uint_as_float(c[i] & 0xffff0000u);
+        }
+    }
+};
+template <>
+struct Elt<float> {
+    static constexpr int EV = 4;
+    __device__ static void unpack(const u32x4& c, float* f) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f[i] = __uint_as_float(c[i]);
+    }
+};
+
+__device__ __forceinline__ u32x4 load16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void store16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+__device__ __forceinline__ float inv_norm(float sumsq) { return sumsq > 0.f ? 1.0f / sqrtf(sumsq) : 0.f; }
+
+// Write chunk `piece` (16 source bytes) of a gathered row: copied bit for
+// bit when the type is kept, widened to fp32 otherwise.
+template <typename T, int D>
+__device__ __forceinline__ void store_chunk(void* dst_row, int piece, const u32x4& c, bool widen) {
+    constexpr int EV = Elt<T>::EV;
+    if (sizeof(T) == 2 && widen) {
+        float f[EV];
+        Elt<T>::unpack(c, f);
+        float* o = static_cast<float*>(dst_row) + piece * EV;
+#pragma unroll
+        for (int q = 0; q < EV / 4; ++q) {
+            u32x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = __float_as_uint(f[4 * q + e]);
+            store16(o + 4 * q, w);
+        }
+    } else {
+        store16(static_cast<T*>(dst_row) + piece * EV, c);
+    }
+}
+
+__device__ __forceinline__ void write_counts(int32_t* counts, int h, int dst_rows, int k, int tid, int nthreads) {
+    if (!counts) return;
+    int32_t* c = counts + (size_t)h * dst_rows;
+    for (int i = tid; i < dst_rows; i += nthreads) c[i] = i < k ? 1 : 0;
+}
+
+// ---- n <= 64: Gram matrix on MFMA, one wave per head ---------------------------
+
+// A lane's share of a 16-row block in MFMA operand order: lane group
+// g = lane >> 4 holds bytes [64 v + 16 g, 64 v + 16 g + 16) of row
+// (lane & 15), for v < NV.  The same registers serve as A (rows of the
+// tile) and as B (columns), since both come from Q.
+template <typename T, int D>
+struct Blk {
+    static constexpr int NV = D * (int)sizeof(T) / 64;
+    u32x4 v[NV];
+};
+
+template <typename T, int D>
+__device__ __forceinline__ void load_blk(Blk<T, D>& b, const T* head, int row0, int n, int lane) {
+    constexpr int EV = Elt<T>::EV;
+    const int r = row0 + (lane & 15);
+    const T* p = head + (size_t)r * D + (lane >> 4) * EV;
+#pragma unroll
+    for (int v = 0; v < Blk<T, D>::NV; ++v) b.v[v] = (r < n) ? load16(p + v * 4 * EV) : u32x4{0u, 0u, 0u, 0u};
+}
+
+template <int D>
+__device__ __forceinline__ void gram_mma(f32x4& acc, const Blk<uint16_t, D>& a, const Blk<uint16_t, D>& b) {
+#pragma unroll
+    for (int v = 0; v < Blk<uint16_t, D>::NV; ++v)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v[v]),
+                                                      __builtin_bit_cast(bf16x8_t, b.v[v]), acc, 0, 0, 0);
+}
+template <int D>
+__device__ __forceinline__ void gram_mma(f32x4& acc, const Blk<float, D>& a, const Blk<float, D>& b) {
+#pragma unroll
+    for (int v = 0; v < Blk<float, D>::NV; ++v)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v[v][e]), __uint_as_float(b.v[v][e]), acc, 0,
+                                                       0, 0);
+}
+
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fminf(v, dev::shfl_xor_f(v, o));
+    return v;
+}
+
+// NB = ceil(n / 16) row blocks.  src is not restrict: dst may be src.
+template <typename T, int D, int NB>
+__global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows, int n, int kmax, int32_t* picks,
+                                                      void* dst, int widen, int dst_rows, int32_t* counts) {
+    constexpr int EV = Elt<T>::EV;
+    constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+    __shared__ float G[16 * NB * kLdg];
+    __shared__ float sinv[16 * NB];
+    const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
+    const int h = blockIdx.x;
+    const T* qh = src + (size_t)h * src_rows * D;
+
+    Blk<T, D> blk[NB];
+    dev::static_for<NB>([&](auto I) { load_blk<T, D>(blk[I], qh, I * 16, n, lane); });
+    // Gram tiles I <= J; each value also goes to its mirror, so the matrix
+    // is exactly symmetric.  Lane (g, c16), register v of tile (I, J) holds
+    // row 16 I + 4 g + v, column 16 J + c16.
+    dev::static_for<NB>([&](auto I) {
+        dev::static_for<NB>([&](auto J) {
+            if constexpr (I <= J) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                gram_mma<D>(acc, blk[I], blk[J]);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int row = 16 * I + 4 * g + v, col = 16 * J + c16;
+                    if (I != J || row <= col) {
+                        G[row * kLdg + col] = acc[v];
+                        G[col * kLdg + row] = acc[v];
+                    }
+                }
+            }
+        });
+    });
+    __syncthreads();
+    // norms from the diagonal, then cosines: G[j][i] *= inv_j * inv_i
+    // (the product of the two inverse norms is the same for both mirrors)
+    const bool live = lane < n;
+    const float inv = live ? inv_norm(G[lane * kLdg + lane]) : 0.f;
+    if (lane < 16 * NB) sinv[lane] = inv;
+    __syncthreads();
+    if (live)
+        for (int j = 0; j < n; ++j) G[j * kLdg + lane] *= sinv[j] * inv;
+    __syncthreads();
+
+    // first pick: argmin of the summed cosines of row `lane` (avg times n)
+    float S = 0.f;
+    if (live)
+        for (int j = 0; j < n; ++j) S += G[j * kLdg + lane];
+    bool done = !live;
+    int mypick = 0;  // lane k keeps pick k
+    for (int k = 0; k < kmax; ++k) {
+        const float key = done ? INFINITY : S;
+        const float mn = wave_min(key);
+        // lowest undone lane at the minimum (never empty: an undone lane
+        // exists while k < min(m, n), and a NaN key counts as a candidate)
+        const unsigned long long bal = __ballot(!done && !(key > mn));
+        const int r = __ffsll(bal) - 1;
+        if (lane == k) mypick = r;
+        if (lane == r) done = true;
+        const float c = G[r * kLdg + lane];
+        if (!done) S = (k == 0) ? c : fmaxf(S, c);
+    }
+    if (picks && lane < kmax) picks[(size_t)h * kmax + lane] = mypick;
+
+    if (dst) {
+        // every chunk of every picked row is loaded (and the loads have
+        // completed) before the first store, so dst may be src
+        constexpr int IT = (16 * NB * CPR + 63) / 64;
+        u32x4 buf[IT];
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            const int c = lane + 64 * it, i = c / CPR, piece = c % CPR;
+            const int row = __shfl(mypick, i < kmax ? i : 0, 64);
+            buf[it] = (i < kmax) ? load16(qh + (size_t)row * D + piece * EV) : u32x4{0u, 0u, 0u, 0u};
+        }
+        dev::wait_all_memory();
+        const size_t drow_bytes = (size_t)D * ((sizeof(T) == 2 && widen) ? 4 : sizeof(T));
+        char* dh = static_cast<char*>(dst) + (size_t)h * dst_rows * drow_bytes;
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            const int c = lane + 64 * it, i = c / CPR, piece = c % CPR;
+            if (i < kmax) store_chunk<T, D>(dh + (size_t)i * drow_bytes, piece, buf[it], widen);
+        }
+    }
+    write_counts(counts, h, dst_rows, kmax, lane, 64);
+}
+
+// ---- n up to 32768: rows streamed per pick, 1024 threads per head -----------------
+
+__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int m) {
+    const unsigned lo = (unsigned)__shfl_xor((int)(unsigned)v, m, 64);
+    const unsigned hi = (unsigned)__shfl_xor((int)(unsigned)(v >> 32), m, 64);
+    return ((unsigned long long)hi << 32) | lo;
+}
+__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long w = shfl_xor_u64(v, o);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+// Order-preserving map of a float to an unsigned key (-0 counts as +0).
+__device__ __forceinline__ unsigned ord_key(float f) {
+    unsigned u = __float_as_uint(f == 0.f ? 0.f : f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Row loads are issued eight 16-byte chunks at a time, so that at most 32
+// registers hold loads in flight next to the per-row state.
+constexpr int kChunkGroup = 8;
+
+// <row, x> for a row of D elements in global memory and D floats in LDS.
+// x is re-read for every row (through an offset the compiler cannot see
+// through): kept in registers across rows it would take D of them.
+template <typename T, int D>
+__device__ __forceinline__ float row_dot(const T* row, const float* x_lds) {
+    constexpr int EV = Elt<T>::EV, CPR = D * (int)sizeof(T) / 16;
+    int off = 0;
+    asm volatile("" : "+v"(off));
+    const float* x = x_lds + off;
+    float p[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c0 = 0; c0 < CPR; c0 += kChunkGroup) {
+#pragma unroll
+        for (int c = c0; c < c0 + kChunkGroup; ++c) {
+            float f[EV];
+            Elt<T>::unpack(load16(row + c * EV), f);
+#pragma unroll
+            for (int e = 0; e < EV; ++e) p[e & 3] = fmaf(f[e], x[c * EV + e], p[e & 3]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    return (p[0] + p[1]) + (p[2] + p[3]);
+}
+
+template <typename T, int D>
+__device__ __forceinline__ float row_sumsq(const T* row) {
+    constexpr int EV = Elt<T>::EV, CPR = D * (int)sizeof(T) / 16;
+    float p[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c0 = 0; c0 < CPR; c0 += kChunkGroup) {
+#pragma unroll
+        for (int c = c0; c < c0 + kChunkGroup; ++c) {
+            float f[EV];
+            Elt<T>::unpack(load16(row + c * EV), f);
+#pragma unroll
+            for (int e = 0; e < EV; ++e) p[e & 3] = fmaf(f[e], f[e], p[e & 3]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    return (p[0] + p[1]) + (p[2] + p[3]);
+}
+
+template <typename T, int D, int RPT>
+__global__ __launch_bounds__(kStreamThreads) void fps_stream_kernel(const T* src, int src_rows, int n, int kmax,
+                                                                    int32_t* picks, void* dst, int widen, int dst_rows,
+                                                                    int32_t* counts) {
+    constexpr int NT = kStreamThreads;
+    constexpr int EV = Elt<T>::EV, CPR = D * (int)sizeof(T) / 16;
+    constexpr int NRG = NT / CPR;  // row groups of the column pass
+    __shared__ __attribute__((aligned(16))) float red[NRG * D];
+    __shared__ __attribute__((aligned(16))) float vec[D];  // mean direction, then the current pick
+    __shared__ float tinv[NT];
+    __shared__ unsigned long long wkey[kStreamWaves];
+    __shared__ float winv[kStreamWaves];
+    __shared__ int spick[kMaxGather];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int h = blockIdx.x;
+    const T* qh = src + (size_t)h * src_rows * D;
+
+    // norms of the owned rows
+    float inv[RPT], S[RPT];
+    unsigned long long done = 0;  // bit i: row t + NT i picked (or absent)
+    dev::static_for<RPT>([&](auto i) {
+        const int j = t + NT * i;
+        inv[i] = (j < n) ? inv_norm(row_sumsq<T, D>(qh + (size_t)j * D)) : 0.f;
+        S[i] = 0.f;
+        if (j >= n) done |= 1ull << i;
+        __builtin_amdgcn_sched_barrier(0);  // one row's loads in flight at a time: no spills
+    });
+
+    // sum of the unit vectors, NT rows at a time: thread (rg, cp) adds chunk
+    // cp of rows rg, rg + NRG, ... of the tile, scaled by their inverse norms
+    {
+        const int cp = t % CPR, rg = t / CPR;
+        float acc[EV];
+#pragma unroll
+        for (int e = 0; e < EV; ++e) acc[e] = 0.f;
+        dev::static_for<RPT>([&](auto i) {
+            if (NT * i < n) {  // uniform
+                tinv[t] = inv[i];
+                __syncthreads();
+                for (int s = rg; s < NT && NT * i + s < n; s += NRG) {
+                    float f[EV];
+                    Elt<T>::unpack(load16(qh + (size_t)(NT * i + s) * D + cp * EV), f);
+                    const float w = tinv[s];
+#pragma unroll
+                    for (int e = 0; e < EV; ++e) acc[e] = fmaf(f[e], w, acc[e]);
+                }
+                __syncthreads();
+            }
+        });
+#pragma unroll
+        for (int e = 0; e < EV; ++e) red[rg * D + cp * EV + e] = acc[e];
+        __syncthreads();
+        if (t < D) {
+            float s = 0.f;
+            for (int r = 0; r < NRG; ++r) s += red[r * D + t];
+            vec[t] = s;
+        }
+        __syncthreads();
+    }
+    // avg_i times n
+    dev::static_for<RPT>([&](auto i) {
+        const int j = t + NT * i;
+        if (j < n) S[i] = row_dot<T, D>(qh + (size_t)j * D, vec) * inv[i];
+        __builtin_amdgcn_sched_barrier(0);
+    });
+    __syncthreads();  // every thread is done with vec before it holds the first pick
+
+    for (int k = 0; k < kmax; ++k) {
+        // (S, j) lexicographic minimum over the unpicked rows
+        unsigned long long best = ~0ull;
+        float binv = 0.f;
+        dev::static_for<RPT>([&](auto i) {
+            if (!((done >> i) & 1ull)) {
+                const unsigned long long key = ((unsigned long long)ord_key(S[i]) << 32) | (unsigned)(t + NT * i);
+                if (key < best) {
+                    best = key;
+                    binv = inv[i];
+                }
+            }
+        });
+        const unsigned long long wbest = wave_min_u64(best);
+        if (wbest == ~0ull) {
+            if (lane == 0) wkey[wave] = wbest;
+        } else if (best == wbest) {  // keys are unique: exactly one lane
+            wkey[wave] = wbest;
+            winv[wave] = binv;
+        }
+        __syncthreads();
+        unsigned long long gb = ~0ull;
+        float rinv = 0.f;
+#pragma unroll
+        for (int w = 0; w < kStreamWaves; ++w) {
+            const unsigned long long x = wkey[w];
+            if (x < gb) {
+                gb = x;
+                rinv = winv[w];
+            }
+        }
+        const int r = (int)(unsigned)gb;  // an unpicked row exists while k < min(m, n)
+        if (t < CPR) {
+            float f[EV];
+            Elt<T>::unpack(load16(qh + (size_t)r * D + t * EV), f);
+#pragma unroll
+            for (int e = 0; e < EV; ++e) vec[t * EV + e] = f[e];
+        }
+        if (t == 0) {
+            if (picks) picks[(size_t)h * kmax + k] = r;
+            if (k < kMaxGather) spick[k] = r;
+        }
+        if (r % NT == t) done |= 1ull << (r / NT);
+        __syncthreads();
+        dev::static_for<RPT>([&](auto i) {
+            if (!((done >> i) & 1ull)) {
+                // the row address is formed here on every pick: hoisted out
+                // of the pick loop, RPT 64-bit addresses would stay live
+                int j = t + NT * i;
+                asm volatile("" : "+v"(j));
+                const float c = row_dot<T, D>(qh + (size_t)j * D, vec) * inv[i] * rinv;
+                S[i] = (k == 0) ? c : fmaxf(S[i], c);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    }
+
+    if (dst) {
+        // all chunks of all picked rows are in registers on every wave
+        // before any wave stores, so dst may be src
+        constexpr int IT = (kMaxGather * CPR + NT - 1) / NT;
+        u32x4 buf[IT];
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            const int c = t + NT * it, i = c / CPR, piece = c % CPR;
+            buf[it] = (i < kmax) ? load16(qh + (size_t)spick[i] * D + piece * EV) : u32x4{0u, 0u, 0u, 0u};
+        }
+        dev::wait_all_memory();
+        __syncthreads();
+        const size_t drow_bytes = (size_t)D * ((sizeof(T) == 2 && widen) ? 4 : sizeof(T));
+        char* dh = static_cast<char*>(dst) + (size_t)h * dst_rows * drow_bytes;
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            const int c = t + NT * it, i = c / CPR, piece = c % CPR;
+            if (i < kmax) store_chunk<T, D>(dh + (size_t)i * drow_bytes, piece, buf[it], widen);
+        }
+    }
+    write_counts(counts, h, dst_rows, kmax, t, NT);
+}
+
+template <typename T, int D>
+hipError_t launch_typed(int H, int n, int kmax, const void* src, int src_rows, int32_t* picks, void* dst, int widen,
+                        int dst_rows, int32_t* counts, hipStream_t s) {
+    const T* q = static_cast<const T*>(src);
+    if (n <= kGramMaxN) {
+        const dim3 grid(H), block(64);
+        switch ((n + 15) / 16) {
+            case 1: hipLaunchKernelGGL((fps_gram_kernel<T, D, 1>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts); break;
+            case 2: hipLaunchKernelGGL((fps_gram_kernel<T, D, 2>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts); break;
+            case 3: hipLaunchKernelGGL((fps_gram_kernel<T, D, 3>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts); break;
+            default: hipLaunchKernelGGL((fps_gram_kernel<T, D, 4>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts); break;
+        }
+        return hipGetLastError();
+    }
+    const int rows_per_thread = (n + kStreamThreads - 1) / kStreamThreads;
+    const dim3 grid(H), block(kStreamThreads);
+#define BKV_FPS_STREAM(R) \
+    hipLaunchKernelGGL((fps_stream_kernel<T, D, R>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts)
+    if (rows_per_thread <= 1) BKV_FPS_STREAM(1);
+    else if (rows_per_thread <= 2) BKV_FPS_STREAM(2);
+    else if (rows_per_thread <= 4) BKV_FPS_STREAM(4);
+    else if (rows_per_thread <= 8) BKV_FPS_STREAM(8);
+    else if (rows_per_thread <= 16) BKV_FPS_STREAM(16);
+    else if (rows_per_thread <= 32) BKV_FPS_STREAM(32);
+    else BKV_FPS_STREAM(kStreamMaxRpt);
+#undef BKV_FPS_STREAM
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_fps(int H, int n, int kmax, int D, int dtype, const void* src, int src_rows, int32_t* picks,
+                      void* dst, int dst_dtype, int dst_rows, int32_t* counts, hipStream_t s) {
+    const int widen = (dst && dtype == BKV_BF16 && dst_dtype == BKV_F32) ? 1 : 0;
+    if (dtype == BKV_BF16)
+        return D == 64 ? launch_typed<uint16_t, 64>(H, n, kmax, src, src_rows, picks, dst, widen, dst_rows, counts, s)
+                       : launch_typed<uint16_t, 128>(H, n, kmax, src, src_rows, picks, dst, widen, dst_rows, counts, s);
+    return D == 64 ? launch_typed<float, 64>(H, n, kmax, src, src_rows, picks, dst, widen, dst_rows, counts, s)
+                   : launch_typed<float, 128>(H, n, kmax, src, src_rows, picks, dst, widen, dst_rows, counts, s);
+}
+
+}  // namespace bkv

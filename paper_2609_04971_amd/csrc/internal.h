@@ -80,4 +80,9 @@ hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hi
 hipError_t launch_compact(const bkv_dims& d, const WsLayout& L, void* K, void* V,
                           const int32_t* kept, void* ws, hipStream_t s);
 
+// FPS over H heads of src [H][src_rows][D], k = min(m, n) picks per head;
+// dst (optional) receives the picked rows, counts (optional) the occupancy.
+hipError_t launch_fps(int H, int n, int kmax, int D, int dtype, const void* src, int src_rows, int32_t* picks,
+                      void* dst, int dst_dtype, int dst_rows, int32_t* counts, hipStream_t s);
+
 }  // namespace bkv

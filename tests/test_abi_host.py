@@ -129,3 +129,59 @@ def test_missing_library_fails_loudly(monkeypatch):
     monkeypatch.setattr(bkv, "LIB_PATH", os.path.join(ROOT, "no-such-dir", "libbkv.so"))
     with pytest.raises(ImportError):
         bkv.validate(good(), bkv.OP_EVICT)
+
+
+# ---- FPS entry points: rejected on the host, or no-ops -------------------------
+_Q = ctypes.c_void_p(0x100000)      # stand-in addresses: only calls that fail
+_Q2 = ctypes.c_void_p(0x900000)     # validation (or are no-ops) are made
+_PK = ctypes.c_void_p(0x200000)
+
+
+def _fps(H=2, n=10, m=4, D=128, dt=None, q=_Q, rows=10, picks=_PK):
+    dt = bkv.BF16 if dt is None else dt
+    return bkv.lib().bkv_fps(H, n, m, D, dt, q, rows, picks, None)
+
+
+def _gather(H=2, n=10, m=4, D=128, dt=None, src=_Q, rows=10, dst=_Q2, ddt=None, drows=10, picks=None,
+            counts=None):
+    dt = bkv.BF16 if dt is None else dt
+    ddt = dt if ddt is None else ddt
+    return bkv.lib().bkv_fps_gather(H, n, m, D, dt, src, rows, dst, ddt, drows, picks, counts, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(D=96), bkv.ERR_SHAPE),
+    (dict(dt=5), bkv.ERR_DTYPE),
+    (dict(n=11), bkv.ERR_SHAPE),                   # more rows than the head holds
+    (dict(n=32769, rows=40000), bkv.ERR_SHAPE),   # above the row limit
+    (dict(H=-1), bkv.ERR_SHAPE),
+    (dict(m=-1), bkv.ERR_SHAPE),
+    (dict(q=None), bkv.ERR_INVALID),
+    (dict(q=ctypes.c_void_p(0x100004)), bkv.ERR_INVALID),  # not 16-byte aligned
+    (dict(picks=None), bkv.ERR_INVALID),
+])
+def test_fps_rejects(kw, code):
+    assert _fps(**kw) == code
+
+
+def test_fps_empty_is_a_no_op():
+    assert _fps(H=0) == bkv.OK
+    assert _fps(n=0) == bkv.OK
+    assert _fps(m=0) == bkv.OK
+    assert _fps(H=0, q=None, picks=None) == bkv.OK
+    assert _gather(m=0, dst=None) == bkv.OK
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=bkv.F32, ddt=bkv.BF16), bkv.ERR_DTYPE),   # narrowing is not offered
+    (dict(ddt=7), bkv.ERR_DTYPE),
+    (dict(n=200, rows=200, m=129, drows=200), bkv.ERR_SHAPE),  # more than 128 gathered rows
+    (dict(m=4, drows=3), bkv.ERR_SHAPE),                # dst too short for the picks
+    (dict(dst=None), bkv.ERR_INVALID),
+    (dict(dst=ctypes.c_void_p(0x100000 + 256)), bkv.ERR_INVALID),  # partial overlap with src
+    (dict(dst=_Q, drows=12), bkv.ERR_INVALID),          # same base, other layout
+    (dict(dst=_Q, ddt=bkv.F32), bkv.ERR_INVALID),       # same base, widened in place
+    (dict(D=64, n=33000, rows=33000), bkv.ERR_SHAPE),
+])
+def test_fps_gather_rejects(kw, code):
+    assert _gather(**kw) == code
