@@ -76,6 +76,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=768,
                     help="(batch, kv-head) pairs in the CPU oracle sample, taken layer by layer")
+    ap.add_argument("--no-fps", action="store_true", help="skip the Continual FPS timings")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -202,11 +203,58 @@ def main():
         "roofline": roofline,
         "setup_s": round(gen_s, 1),
     }
+    del layers
+    torch.cuda.empty_cache()
+    if not args.no_fps:
+        out["continual_fps"] = fps_measure(w, dev)
     if not args.no_cpu_baseline:
-        del layers
-        torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_heads)
     print(json.dumps(out), flush=True)
+
+
+def fps_measure(w, dev, reps=20):
+    """Continual FPS (Section 4.2; Appendix D.1, Algorithm 1), timed with HIP
+    events on the launch stream, outside the eviction step:
+      * continual_compress: every query head of every layer (36 x 16 x 32
+        buffers) compresses its B_Q^max = 32 pre-RoPE queries to B_Q^min = 16
+        in place, one launch (all layers fill on the same decode step);
+      * prefill_init: FPS of a 1024-token prompt's queries per query head of
+        one layer, the 16 picks written into the heads' query buffers.
+    Algorithmic bytes per launch: every row read once, the picked rows and
+    the pick indices written once."""
+    import torch
+
+    import paper_2609_04971_amd as bkv
+    from paper_2609_04971_amd import synth
+
+    res = {}
+    cases = (("continual_compress", w.B * w.layers, 32, 16, True), ("prefill_init", w.B, 1024, 16, False))
+    for name, B, n, m, in_place in cases:
+        src = synth.query_stream(w.with_(B=B), n, seed=77, device=dev)
+        dst = src if in_place else torch.zeros(B, w.Hq, 32, w.D, dtype=src.dtype, device=dev)
+        picks = torch.empty(B, w.Hq, m, dtype=torch.int32, device=dev)
+        for _ in range(2):
+            bkv.fps_gather(src, m, dst=dst, picks=picks)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            bkv.fps_gather(src, m, dst=dst, picks=picks)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        H = B * w.Hq
+        k = min(m, n)
+        nbytes = H * (n * w.D * 2 + k * w.D * 2 + k * 4)
+        gbs = nbytes / (us * 1e-6) / 1e9
+        res[name] = {"heads": H, "n": n, "m": m, "in_place": in_place, "us": round(us, 2),
+                     "kernel": ("fps_gram_kernel<unsigned short, 128, 2>" if n <= 64
+                                else "fps_stream_kernel<unsigned short, 128, 2>"),
+                     "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                  "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes}}
+        del src, dst, picks
+        torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(w, n_heads):
