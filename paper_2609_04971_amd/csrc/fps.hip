@@ -8,9 +8,9 @@
 //  - fps_gram_kernel, n <= 64, one wave.  These are the buffers of the
 //    continual path (B_Q^max = n_beacon + n_recent rows).  The whole Gram
 //    matrix Q Q^T of the head comes from MFMA (exact bf16 products, fp32
-//    sums; fp32 input uses the fp32 MFMA), its diagonal gives the norms, and
-//    it is normalised to cosines in LDS once.  avg_i is then a column sum,
-//    and each pick costs one LDS read per lane and a wave argmin.
+//    sums; fp32 input uses the fp32 MFMA) and its diagonal gives the norms.
+//    avg_i is then a column sum, and each pick costs one LDS read per lane
+//    and a wave argmin on DPP and scalar instructions.
 //  - fps_stream_kernel, n up to 32768, 1024 threads.  Prefill-sized sets.
 //    Thread t owns rows j = t + 1024 i and keeps their S_j and 1/|q_j| in
 //    registers.  avg_i uses the regrouped sum
@@ -134,20 +134,33 @@ __device__ __forceinline__ void gram_mma(f32x4& acc, const Blk<float, D>& a, con
                                                        0, 0);
 }
 
+// min(v, v of the lane that DPP control CTRL names); all 64 lanes active.
+template <int CTRL>
+__device__ __forceinline__ float dpp_min(float v) {
+    const int w = __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf, false);
+    return fminf(v, __int_as_float(w));
+}
+
+__device__ __forceinline__ float lane_value(float v, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Minimum over the wave, the same in every lane: swaps within quads, then
+// the half-row and row mirrors give each 16-lane row its minimum (DPP, no
+// LDS round trip), and the four row minima are combined as scalars.
 __device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fminf(v, dev::shfl_xor_f(v, o));
-    return v;
+    v = dpp_min<0xb1>(v);   // quad_perm [1, 0, 3, 2]
+    v = dpp_min<0x4e>(v);   // quad_perm [2, 3, 0, 1]
+    v = dpp_min<0x141>(v);  // row_half_mirror
+    v = dpp_min<0x140>(v);  // row_mirror
+    return fminf(fminf(lane_value(v, 0), lane_value(v, 16)), fminf(lane_value(v, 32), lane_value(v, 48)));
 }
 
 // NB = ceil(n / 16) row blocks.  src is not restrict: dst may be src.
 template <typename T, int D, int NB>
 __global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows, int n, int kmax, int32_t* picks,
                                                       void* dst, int widen, int dst_rows, int32_t* counts) {
-    constexpr int EV = Elt<T>::EV;
-    constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
     __shared__ float G[16 * NB * kLdg];
-    __shared__ float sinv[16 * NB];
     const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
     const int h = blockIdx.x;
     const T* qh = src + (size_t)h * src_rows * D;
@@ -174,20 +187,16 @@ __global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows
         });
     });
     __syncthreads();
-    // norms from the diagonal, then cosines: G[j][i] *= inv_j * inv_i
-    // (the product of the two inverse norms is the same for both mirrors)
+    // Lane i keeps 1/|q_i| (from the diagonal); cos(q_i, q_j) is formed as
+    // G[j][i] * inv_i * inv_j when it is needed, with inv_j read from lane j.
     const bool live = lane < n;
     const float inv = live ? inv_norm(G[lane * kLdg + lane]) : 0.f;
-    if (lane < 16 * NB) sinv[lane] = inv;
-    __syncthreads();
-    if (live)
-        for (int j = 0; j < n; ++j) G[j * kLdg + lane] *= sinv[j] * inv;
-    __syncthreads();
 
     // first pick: argmin of the summed cosines of row `lane` (avg times n)
     float S = 0.f;
-    if (live)
-        for (int j = 0; j < n; ++j) S += G[j * kLdg + lane];
+#pragma unroll 8
+    for (int j = 0; j < n; ++j) S = fmaf(G[j * kLdg + lane], lane_value(inv, j), S);
+    S *= inv;
     bool done = !live;
     int mypick = 0;  // lane k keeps pick k
     for (int k = 0; k < kmax; ++k) {
@@ -199,29 +208,37 @@ __global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows
         const int r = __ffsll(bal) - 1;
         if (lane == k) mypick = r;
         if (lane == r) done = true;
-        const float c = G[r * kLdg + lane];
+        const float c = G[r * kLdg + lane] * inv * lane_value(inv, r);
         if (!done) S = (k == 0) ? c : fmaxf(S, c);
     }
     if (picks && lane < kmax) picks[(size_t)h * kmax + lane] = mypick;
 
     if (dst) {
-        // every chunk of every picked row is loaded (and the loads have
-        // completed) before the first store, so dst may be src
-        constexpr int IT = (16 * NB * CPR + 63) / 64;
-        u32x4 buf[IT];
-#pragma unroll
-        for (int it = 0; it < IT; ++it) {
-            const int c = lane + 64 * it, i = c / CPR, piece = c % CPR;
-            const int row = __shfl(mypick, i < kmax ? i : 0, 64);
-            buf[it] = (i < kmax) ? load16(qh + (size_t)row * D + piece * EV) : u32x4{0u, 0u, 0u, 0u};
-        }
-        dev::wait_all_memory();
+        // The picked rows are still in the operand registers: lane (g, c)
+        // writes bytes [64 v + 16 g, +16) of destination rows c, c + 16, ...,
+        // which sit in the same lane group g of the source row's block, so
+        // a cross-lane read (one per block and dword) fetches them.  Nothing
+        // is re-read from memory, and every store follows all of the loads,
+        // so dst may be src.
+        constexpr int NV = Blk<T, D>::NV;
         const size_t drow_bytes = (size_t)D * ((sizeof(T) == 2 && widen) ? 4 : sizeof(T));
         char* dh = static_cast<char*>(dst) + (size_t)h * dst_rows * drow_bytes;
+        for (int i0 = 0; i0 < kmax; i0 += 16) {
+            const int i = i0 + c16;
+            const int src_row = __shfl(mypick, i < kmax ? i : kmax - 1, 64);
+            const int src_lane = (g << 4) | (src_row & 15), src_blk = src_row >> 4;
 #pragma unroll
-        for (int it = 0; it < IT; ++it) {
-            const int c = lane + 64 * it, i = c / CPR, piece = c % CPR;
-            if (i < kmax) store_chunk<T, D>(dh + (size_t)i * drow_bytes, piece, buf[it], widen);
+            for (int v = 0; v < NV; ++v) {
+                u32x4 x = {0u, 0u, 0u, 0u};
+                dev::static_for<NB>([&](auto I) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const unsigned y = (unsigned)__shfl((int)blk[I].v[v][e], src_lane, 64);
+                        x[e] = (src_blk == I) ? y : x[e];
+                    }
+                });
+                if (i < kmax) store_chunk<T, D>(dh + (size_t)i * drow_bytes, 4 * v + g, x, widen);
+            }
         }
     }
     write_counts(counts, h, dst_rows, kmax, lane, 64);
@@ -229,18 +246,28 @@ __global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows
 
 // ---- n up to 32768: rows streamed per pick, 1024 threads per head -----------------
 
-__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int m) {
-    const unsigned lo = (unsigned)__shfl_xor((int)(unsigned)v, m, 64);
-    const unsigned hi = (unsigned)__shfl_xor((int)(unsigned)(v >> 32), m, 64);
-    return ((unsigned long long)hi << 32) | lo;
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_min_u32(unsigned v) {
+    const unsigned w = (unsigned)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+    return w < v ? w : v;
 }
+
+__device__ __forceinline__ unsigned wave_min_u32(unsigned v) {
+    v = dpp_min_u32<0xb1>(v);
+    v = dpp_min_u32<0x4e>(v);
+    v = dpp_min_u32<0x141>(v);
+    v = dpp_min_u32<0x140>(v);
+    const unsigned a = (unsigned)__builtin_amdgcn_readlane((int)v, 0), b = (unsigned)__builtin_amdgcn_readlane((int)v, 16);
+    const unsigned c = (unsigned)__builtin_amdgcn_readlane((int)v, 32), d = (unsigned)__builtin_amdgcn_readlane((int)v, 48);
+    return min(min(a, b), min(c, d));
+}
+
+// Lexicographic minimum of 64-bit keys over the wave (all lanes active):
+// the high words first, then the low words of the lanes that hold it.
 __device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long w = shfl_xor_u64(v, o);
-        v = w < v ? w : v;
-    }
-    return v;
+    const unsigned hi = wave_min_u32((unsigned)(v >> 32));
+    const unsigned lo = wave_min_u32((unsigned)(v >> 32) == hi ? (unsigned)v : 0xffffffffu);
+    return ((unsigned long long)hi << 32) | lo;
 }
 // Order-preserving map of a float to an unsigned key (-0 counts as +0).
 __device__ __forceinline__ unsigned ord_key(float f) {

@@ -648,40 +648,57 @@ __device__ __forceinline__ void read_key_tile(Op<uint16_t, D>& op, const uint16_
 // Running (max, sum) of one S item over one staged group of 32 keys.
 // Keys at or past N (only in a head's last group, TAIL) enter with the
 // accumulator seeded at -inf, so they add exp2(-inf) = 0.
+//
+// Software-pipelined by one row tile: the MFMAs of tile rt + 1 are issued
+// in the same scheduling region as the exp/max work on tile rt and
+// interleaved with it (one MFMA, then four VALU instructions), so the
+// matrix core is not left idle while the wave waits on its results.  Only
+// two tiles of accumulators are live at a time; hoisting more would spill
+// the registers that hold the rows.
 template <int D, int RT, bool TAIL>
 __device__ __forceinline__ void stats_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr, float s2,
                                             float* m, float* z, int c16, int g) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-        f32x4 acc[2];
+    f32x4 acc[2][2];
+    auto issue = [&](int rt, f32x4* a) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) acc[t][v] = (!TAIL || kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
-            mma(acc[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
+            for (int v = 0; v < 4; ++v) a[t][v] = (!TAIL || kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
+            mma(a[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
         }
-        const float gm = fmaxf(fmaxf(fmaxf(acc[0][0], acc[0][1]), fmaxf(acc[0][2], acc[0][3])),
-                               fmaxf(fmaxf(acc[1][0], acc[1][1]), fmaxf(acc[1][2], acc[1][3])));
+    };
+    issue(0, acc[0]);
+    dev::static_for<RT>([&](auto rt) {
+        if constexpr (rt + 1 < RT) issue(rt + 1, acc[(rt + 1) & 1]);
+        f32x4* a = acc[rt & 1];
+        const float gm = fmaxf(fmaxf(fmaxf(a[0][0], a[0][1]), fmaxf(a[0][2], a[0][3])),
+                               fmaxf(fmaxf(a[1][0], a[1][1]), fmaxf(a[1][2], a[1][3])));
         const float mnew = fmaxf(m[rt], gm * s2);
         const float ms = (mnew == -INFINITY) ? 0.f : mnew;  // no valid key yet: sums stay 0
         float zz = z[rt] * fast_exp2(m[rt] - ms);
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(acc[t][v], s2, -ms));
+            for (int v = 0; v < 4; ++v) zz += fast_exp2(__builtin_fmaf(a[t][v], s2, -ms));
         z[rt] = zz;
         m[rt] = mnew;
-        // one row tile at a time: hoisting later tiles' MFMAs would keep
-        // their accumulators live and spill the registers that hold the rows
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // four VALU
+        }
         __builtin_amdgcn_sched_barrier(0);
-    }
+    });
 }
 
 // Scores of one F item's staged group of 32 keys: per key the maximum over
 // rows, written straight out (64 contiguous bytes per 16-key tile).
+// Pipelined like stats_group; each tile's -lse seed is read from LDS two
+// tiles ahead (re-read every group through an offset the compiler cannot
+// hoist: kept for the whole item these would hold 4 * RT registers).
 template <int D, int RT>
 __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr,
                                             const float* nlse, float* out, float s2ln2, int c16, int g) {
@@ -689,21 +706,36 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
     float best[2] = {-INFINITY, -INFINITY};
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-        // re-read every group: hoisted out of the key loop these would hold
-        // 4 * RT more registers for the whole item
+    f32x4 acc[2][2];
+    f32x4 cn[2];
+    auto load_c = [&](int rt) {
         int off = rt * 16 + 4 * g;
         asm volatile("" : "+v"(off));
-        const f32x4 c0 = *reinterpret_cast<const f32x4*>(nlse + off);
+        return *reinterpret_cast<const f32x4*>(nlse + off);
+    };
+    auto issue = [&](int rt, f32x4* a, const f32x4& c0) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            f32x4 acc = c0;
-            mma(acc, yr[rt], kop[t]);  // rows = observation rows, columns = keys
-            best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
+            a[t] = c0;
+            mma(a[t], yr[rt], kop[t]);  // rows = observation rows, columns = keys
+        }
+    };
+    cn[0] = load_c(0);
+    if constexpr (RT > 1) cn[1] = load_c(1);
+    issue(0, acc[0], cn[0]);
+    dev::static_for<RT>([&](auto rt) {
+        if constexpr (rt + 2 < RT) cn[rt & 1] = load_c(rt + 2);
+        if constexpr (rt + 1 < RT) issue(rt + 1, acc[(rt + 1) & 1], cn[(rt + 1) & 1]);
+        f32x4* a = acc[rt & 1];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) best[t] = fmaxf(best[t], fmaxf(fmaxf(a[t][0], a[t][1]), fmaxf(a[t][2], a[t][3])));
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // one VALU
         }
         __builtin_amdgcn_sched_barrier(0);
-    }
+    });
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
         float b = best[t];
