@@ -476,16 +476,28 @@ __device__ __forceinline__ int head_of_block(const Args& a, int b) {
 
 // ---- work-item protocol shared by both paths --------------------------------
 // Take the next work ticket of head h (tickets below nch are S items, the
-// rest F items); false if the workspace stamp or control line is bad.
-__device__ __forceinline__ bool take_ticket(const Args& a, int h, int* s_ticket, int* s_ok) {
-    int* hc = a.hctl + (size_t)h * kHcWords;
+// rest F items); false if the workspace stamp or control line is bad.  The
+// request is issued first and completed separately, so that loads issued in
+// between (the fast path's rows) are in flight while the atomic returns; the
+// ticket is taken before the stamp is known, which only matters when the
+// item then does nothing and reports the bad stamp.
+struct TicketReq {
+    int t;
+    dev::u32x4 hdr;  // magic, P, budget, error bits
+};
+__device__ __forceinline__ TicketReq request_ticket(const Args& a, int h) {
+    TicketReq r{0, {0u, 0u, 0u, 0u}};
     if (threadIdx.x == 0) {
-        int ok = dev::stamp_ok(a.hdr, a.P, a.budget);
-        if (ok) {
-            const int t = dev::fetch_add_relaxed(hc + kHcScTicket, 1);
-            *s_ticket = t;
-            if (t >= 2 * a.nch) ok = 0;  // control line was not clear: do nothing
-        }
+        r.t = dev::fetch_add_relaxed(a.hctl + (size_t)h * kHcWords + kHcScTicket, 1);
+        r.hdr = *reinterpret_cast<const dev::u32x4*>(a.hdr);  // one load, checked on completion
+    }
+    return r;
+}
+__device__ __forceinline__ bool complete_ticket(const Args& a, const TicketReq& r, int* s_ticket, int* s_ok) {
+    if (threadIdx.x == 0) {
+        int ok = r.hdr[kHdrMagic] == kWsMagic && (int)r.hdr[kHdrP] == a.P && (int)r.hdr[kHdrBudget] == a.budget;
+        *s_ticket = r.t;
+        if (ok && r.t >= 2 * a.nch) ok = 0;  // control line was not clear: do nothing
         if (!ok) dev::raise_error(a.hdr, kErrStamp);
         *s_ok = ok;
     }
@@ -512,7 +524,7 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
     __shared__ Smem<T, D> sm;
     __shared__ int s_ticket, s_ok, s_flag;
     const int h = head_of_block(a, blockIdx.x);
-    if (!take_ticket(a, h, &s_ticket, &s_ok)) return;
+    if (!complete_ticket(a, request_ticket(a, h), &s_ticket, &s_ok)) return;
     if (s_ticket < a.nch)
         stats_item<T, D, KGN>(a, h, s_ticket, sm, &s_flag);
     else
@@ -867,9 +879,10 @@ __global__ __launch_bounds__(kThreads, 2) void fast_score_kernel(Args a) {
     __shared__ StageBuf<D> sb;
     __shared__ int s_ticket, s_ok, s_flag;
     const int h = head_of_block(a, blockIdx.x);
+    const TicketReq req = request_ticket(a, h);
     Op<uint16_t, D> yr[RT];
     load_rows<D, RT>(a, h, yr, threadIdx.x & 63);  // in flight with the ticket
-    if (!take_ticket(a, h, &s_ticket, &s_ok)) {
+    if (!complete_ticket(a, req, &s_ticket, &s_ok)) {
         wait_vmem<0>();
         return;
     }
