@@ -93,10 +93,11 @@ size_t bkv_workspace_bytes(const bkv_dims* d, int32_t op);
 
 /* Enqueue the initialisation of a workspace: clears its control block and
  * stamps it with (B*Hkv, budget).  Required once after allocation, again
- * whenever B*Hkv or budget change, and after a BKV_ERR_DEVICE.  Kernels
- * leave the control block clear when they finish, so calls in between need
- * nothing.  A kernel that finds a workspace not stamped for its dims does no
- * work and raises BKV_ERR_DEVICE. */
+ * whenever B*Hkv or budget change, and after a BKV_ERR_DEVICE.  Calls in
+ * between need nothing: every score launch resets its own control words
+ * before its work starts, and compaction leaves its words clear.  A kernel
+ * that finds a workspace not stamped for its dims does no work and raises
+ * BKV_ERR_DEVICE. */
 bkv_status bkv_workspace_init(const bkv_dims* d, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Synchronise `stream`, then report the device-side error word of `ws`:

@@ -11,7 +11,9 @@
 namespace bkv {
 
 // ---- workspace --------------------------------------------------------------
-// Control block (must be all-zero at rest except the stamp), then data.
+// Control block (zeroed by init except the stamp; the score words are also
+// reset by every score launch before it starts, the compaction words are
+// left zero by every compaction), then data.
 // The control block's size and offsets depend only on P = B*Hkv and budget,
 // so one initialised workspace stays valid while N, W or C change.
 constexpr uint32_t kWsMagic = 0x424b5631u;  // "BKV1"
@@ -28,7 +30,6 @@ enum HdrWord : int {
 // different heads never contend for one address.
 enum HeadWord : int {
     kHcScTicket = 0,  // score: work ticket within the head
-    kHcScDone = 1,    // score: work items of the head finished
     kHcP1Count = 2,   // score: statistics items of the head finished
     kHcReady = 3,     // score: the head's row normalisers are published
     kHcCpTicket = 4,  // compaction: work ticket within the head

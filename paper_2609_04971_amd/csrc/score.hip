@@ -242,18 +242,18 @@ __device__ void fold_and_publish(const Args& a, int h, const int* act, int nact,
     for (int r = tid; r < a.R_pad_max; r += kThreads) {
         float mm = -INFINITY, zz = 0.f;
         if (r < R) {
-            // sixteen chunks' statistics in flight at once: these are memory
-            // round trips on the head's critical path
-            for (int c0 = 0; c0 < a.nch; c0 += 16) {
-                float pm[16], pz[16];
+            // 32 chunks' statistics in flight at once (all of a 32K head):
+            // these are memory round trips on the head's critical path
+            for (int c0 = 0; c0 < a.nch; c0 += 32) {
+                float pm[32], pz[32];
 #pragma unroll
-                for (int u = 0; u < 16; ++u) {
+                for (int u = 0; u < 32; ++u) {
                     const size_t i = hb + (size_t)min(c0 + u, a.nch - 1) * a.R_pad_max + r;
                     pm[u] = dev::ld_coherent(a.part_m + i);
                     pz[u] = dev::ld_coherent(a.part_z + i);
                 }
 #pragma unroll
-                for (int u = 0; u < 16; ++u)
+                for (int u = 0; u < 32; ++u)
                     if (c0 + u < a.nch) merge_mz(mm, zz, pm[u], pz[u]);
             }
         }
@@ -505,15 +505,23 @@ __device__ __forceinline__ bool complete_ticket(const Args& a, const TicketReq& 
     return *s_ok != 0;
 }
 
-// The head's last workgroup to finish clears its control words.
-__device__ __forceinline__ void finish_item(const Args& a, int h, int* s_flag) {
-    int* hc = a.hctl + (size_t)h * kHcWords;
-    __syncthreads();
-    if (threadIdx.x == 0) *s_flag = (dev::fetch_add_relaxed(hc + kHcScDone, 1) == 2 * a.nch - 1);
-    __syncthreads();
-    if (*s_flag && threadIdx.x == 0) {
+// Clear head h's score control words (thread 0).  Every score launch does
+// this for all heads in a kernel of its own, before any work item takes a
+// ticket, so work items never wait at the end to find the head's last one.
+__device__ __forceinline__ void reset_head_control(const Args& a, int h) {
+    if (threadIdx.x == 0) {
+        int* hc = a.hctl + (size_t)h * kHcWords;
         dev::st_flag(hc + kHcScTicket, 0);
-        dev::st_flag(hc + kHcScDone, 0);
+        dev::st_flag(hc + kHcP1Count, 0);
+        dev::st_flag(hc + kHcReady, 0);
+    }
+}
+
+__global__ void reset_control_kernel(Args a) {
+    const int h = blockIdx.x * blockDim.x + threadIdx.x;
+    if (h < a.P) {
+        int* hc = a.hctl + (size_t)h * kHcWords;
+        dev::st_flag(hc + kHcScTicket, 0);
         dev::st_flag(hc + kHcP1Count, 0);
         dev::st_flag(hc + kHcReady, 0);
     }
@@ -529,7 +537,6 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
         stats_item<T, D, KGN>(a, h, s_ticket, sm, &s_flag);
     else
         final_item<T, D, KGN>(a, h, s_ticket - a.nch, sm, &s_flag);
-    finish_item(a, h, &s_flag);
 }
 
 // ---- fast path: bf16 cache, at most 144 observation rows -----------------
@@ -593,6 +600,7 @@ __global__ __launch_bounds__(kThreads) void rows_kernel(Args a) {
     __shared__ int act[kMaxC];
     __shared__ int nact;
     const int h = blockIdx.x, tid = threadIdx.x;
+    reset_head_control(a, h);
     active_slots(a, h, act, &nact);
     build_rows<uint16_t, D, LD>(a, h, 0, a.R_pad_max, act, nact, y);
     __syncthreads();
@@ -891,7 +899,6 @@ __global__ __launch_bounds__(kThreads, 2) void fast_score_kernel(Args a) {
         fast_stats<D, RT>(a, h, ticket, sm, sa, sb, yr, &s_flag);
     else
         fast_final<D, RT>(a, h, ticket - a.nch, sm, sa, sb, yr, &s_flag);
-    finish_item(a, h, &s_flag);
 }
 
 template <int D, int RT>
@@ -918,6 +925,7 @@ hipError_t launch_fast(const Args& a, hipStream_t s) {
 
 template <typename T, int D, int KGN>
 hipError_t launch_t(const Args& a, hipStream_t s) {
+    hipLaunchKernelGGL(reset_control_kernel, dim3((a.P + 255) / 256), dim3(256), 0, s, a);
     hipLaunchKernelGGL((score_kernel<T, D, KGN>), dim3(a.total), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
