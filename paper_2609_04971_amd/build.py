@@ -31,10 +31,14 @@ FLAGS = [
 
 
 # Per-file additions.  The score kernels never produce or consume NaN, so
-# fmax needs no quieting of its inputs there; and their atomics are made by
-# one thread, so the wave-aggregating rewrite of atomics only adds a scan
-# that needs the result at once (which stalls the loads issued after it).
-FILE_FLAGS = {"score.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+# fmax needs no quieting of its inputs there.  The score and compaction
+# atomics are made by one thread, so the wave-aggregating rewrite of atomics
+# only adds a scan that needs the result at once (which stalls the loads
+# issued after it).
+FILE_FLAGS = {
+    "score.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
+    "compact.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
+}
 
 
 def _compile(src, resource_usage):

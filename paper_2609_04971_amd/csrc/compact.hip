@@ -47,11 +47,13 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
     const int h = blockIdx.x / a.nseg;
     int* hc = a.hctl + (size_t)h * kHcWords;
     if (tid == 0) {
-        s_ok = dev::stamp_ok(a.hdr, a.P, a.budget);
-        if (s_ok)
-            s_ticket = dev::fetch_add_relaxed(hc + kHcCpTicket, 1);
-        else
-            dev::raise_error(a.hdr, kErrStamp);
+        // ticket and stamp requested together (the stamp as one 16-byte
+        // load); a ticket taken on a bad workspace is never used
+        const int t = dev::fetch_add_relaxed(hc + kHcCpTicket, 1);
+        const dev::u32x4 hdr = *reinterpret_cast<const dev::u32x4*>(a.hdr);
+        s_ok = hdr[kHdrMagic] == kWsMagic && (int)hdr[kHdrP] == a.P && (int)hdr[kHdrBudget] == a.budget;
+        s_ticket = t;
+        if (!s_ok) dev::raise_error(a.hdr, kErrStamp);
         s_move = 0;
         s_bad = 0;
         s_wait_ok = 1;
