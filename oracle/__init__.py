@@ -61,6 +61,13 @@ def _load():
     lib.orc_evict_head.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p,
                                    _p, _f, _p, _p, _p]
     lib.orc_evict_head.restype = _i
+    lib.orc_score_ex.argtypes = [_i, _i, _i, _p, _p, _i, ctypes.c_double, _i, _p, _p, _p]
+    lib.orc_score_ex.restype = _i
+    lib.orc_score_head_ex.argtypes = [_i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _f, _i, _i, _p, _p]
+    lib.orc_score_head_ex.restype = _i
+    lib.orc_evict_head_ex.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p,
+                                      _p, _f, _i, _i, _p, _p, _p]
+    lib.orc_evict_head_ex.restype = _i
     _lib = lib
     return lib
 
@@ -145,9 +152,13 @@ def rope_row(beta, cos_t=None, sin_t=None, to_bf16: bool = False):
     return out
 
 
-def score_rows(Y, Khead, scale: float):
+_AGG = {"max": 0, "mean": 1}
+
+
+def score_rows(Y, Khead, scale: float, agg: str = "max", limit=None):
     """(a3) on explicit float64 rows Y [R,D] and keys Khead [N,D] (fp32 or
-    bf16 raw); returns (lse [R], s [N])."""
+    bf16 raw); returns (lse [R], s [N]).  agg "mean" takes Eq. (6)'s mean
+    form; limit [R] (optional) lets row r see keys j <= limit[r] only."""
     lib = _load()
     Yd = np.ascontiguousarray(Y, dtype=np.float64)
     k, dt = _raw(Khead)
@@ -155,14 +166,16 @@ def score_rows(Y, Khead, scale: float):
     N, D = k.shape
     lse = np.zeros(max(R, 1), np.float64)
     s = np.zeros(max(N, 1), np.float64)
-    rc = lib.orc_score(R, N, D, _ptr(Yd), _ptr(k), dt, float(scale), _ptr(lse), _ptr(s))
+    lim = None if limit is None else np.ascontiguousarray(limit, dtype=np.int32)
+    rc = lib.orc_score_ex(R, N, D, _ptr(Yd), _ptr(k), dt, float(scale), _AGG[agg],
+                          None if lim is None else _ptr(lim), _ptr(lse), _ptr(s))
     if rc:
         raise RuntimeError(f"orc_score failed ({rc})")
     return lse[:R], s[:N]
 
 
 def score(K, q_win, beacons, counts, N: int, rope_cos=None, rope_sin=None, scale: float = 0.0,
-          heads=None, threads: int = 1):
+          heads=None, threads: int = 1, agg: str = "max", causal: bool = False):
     """(a2)+(a3) for every (b, kv-head) or the listed `heads` [(b, h), ...].
     K [B,Hkv,N_cap,D], q_win [B,Hq,W,D] post-RoPE, beacons [B,Hkv,C,D] fp32,
     counts [B,Hkv,C].  Returns (scores [B,Hkv,N] float64, row_lse
@@ -190,10 +203,11 @@ def score(K, q_win, beacons, counts, N: int, rope_cos=None, rope_sin=None, scale
         b, h = bh
         s_h = np.zeros(max(N, 1), np.float64)
         l_h = np.zeros(max(C + G * W, 1), np.float64)
-        rc = lib.orc_score_head(dt, D, N, C, G, W, _ptr(k, (b * Hkv + h) * Ncap * D),
-                                _ptr(qw, (b * Hq + h * G) * W * D), _ptr(bc, (b * Hkv + h) * C * D),
-                                _ptr(cn, (b * Hkv + h) * C), None if cs is None else _ptr(cs),
-                                None if sn is None else _ptr(sn), float(scale), _ptr(l_h), _ptr(s_h))
+        rc = lib.orc_score_head_ex(dt, D, N, C, G, W, _ptr(k, (b * Hkv + h) * Ncap * D),
+                                   _ptr(qw, (b * Hq + h * G) * W * D), _ptr(bc, (b * Hkv + h) * C * D),
+                                   _ptr(cn, (b * Hkv + h) * C), None if cs is None else _ptr(cs),
+                                   None if sn is None else _ptr(sn), float(scale), _AGG[agg], int(bool(causal)),
+                                   _ptr(l_h), _ptr(s_h))
         if rc:
             raise RuntimeError(f"orc_score_head failed ({rc})")
         scores[b, h] = s_h[:N]
@@ -248,7 +262,8 @@ def compact(K, V, kept):
 
 
 def evict(K, V, q_win, beacons, counts, N: int, budget: int, W: int, n_prefix: int = 0,
-          rope_cos=None, rope_sin=None, scale: float = 0.0, heads=None, threads: int = 1):
+          rope_cos=None, rope_sin=None, scale: float = 0.0, heads=None, threads: int = 1, agg: str = "max",
+          causal: bool = False):
     """(a6) = (a2)->(a5) for every head or the listed `heads`, on copies.
     Returns dict(K, V (raw numpy, compacted), scores, row_lse, kept); heads
     not listed keep their input rows and read NaN / -1."""
@@ -278,12 +293,12 @@ def evict(K, V, q_win, beacons, counts, N: int, budget: int, W: int, n_prefix: i
         s_h = np.zeros(max(N, 1), np.float64)
         l_h = np.zeros(max(C + G * W, 1), np.float64)
         kp = np.zeros(max(nk, 1), np.int32)
-        n = lib.orc_evict_head(dt, D, N, C, G, W, budget, n_prefix,
-                               _ptr(k, (b * Hkv + h) * Ncap * D), _ptr(v, (b * Hkv + h) * Ncap * D),
-                               _ptr(qw, (b * Hq + h * G) * W * D), _ptr(bc, (b * Hkv + h) * C * D),
-                               _ptr(cn, (b * Hkv + h) * C), None if cs is None else _ptr(cs),
-                               None if sn is None else _ptr(sn), float(scale), _ptr(l_h), _ptr(s_h),
-                               _ptr(kp))
+        n = lib.orc_evict_head_ex(dt, D, N, C, G, W, budget, n_prefix,
+                                  _ptr(k, (b * Hkv + h) * Ncap * D), _ptr(v, (b * Hkv + h) * Ncap * D),
+                                  _ptr(qw, (b * Hq + h * G) * W * D), _ptr(bc, (b * Hkv + h) * C * D),
+                                  _ptr(cn, (b * Hkv + h) * C), None if cs is None else _ptr(cs),
+                                  None if sn is None else _ptr(sn), float(scale), _AGG[agg], int(bool(causal)),
+                                  _ptr(l_h), _ptr(s_h), _ptr(kp))
         if n < 0:
             raise RuntimeError(f"orc_evict_head failed ({n})")
         scores[b, h] = s_h[:N]

@@ -203,8 +203,20 @@ int orc_assemble_rows(int dtype, int D, int C, int G, int W, const float* beacon
  *   s_j   = max_r (l_rj - lse_r),  so exp(s_j) = max_r w_rj.
  * With no rows at all every s_j is -inf.
  * ------------------------------------------------------------------------ */
-int orc_score(int R, int N, int D, const double* Y, const void* Khead, int dtype, double scale,
-              double* lse, double* s) {
+/* Scoring variants (the next step after the max form).
+ *
+ * agg = 1 takes the other aggregation Eq. (6) defines, the mean over the
+ * observation queries, s_j^mean = (1/R) sum_r w_rj (the paper ablates it
+ * against the max in Table 2), kept in the log domain as
+ *   s_j = ln((1/R) sum_r exp(l_rj - lse_r)).
+ * With `limit` given, row r sees only the keys j <= limit[r] (a causal
+ * restriction for recent queries): its lse runs over those keys alone and
+ * its weight on every later key is 0.  A row that sees no key has
+ * lse = -inf and weight 0 everywhere; R still counts it in the mean.  A key
+ * no row sees scores -inf.  agg = 0, limit = NULL is orc_score.
+ */
+int orc_score_ex(int R, int N, int D, const double* Y, const void* Khead, int dtype, double scale, int agg,
+                 const int32_t* limit, double* lse, double* s) {
     if (R == 0) {
         for (int j = 0; j < N; ++j) s[j] = -INFINITY;
         return 0;
@@ -224,54 +236,81 @@ int orc_score(int R, int N, int D, const double* Y, const void* Khead, int dtype
             logit[(size_t)r * N + j] = scale * dot;
         }
     }
+    /* keys j < seen(r) are the ones row r sees */
+#define ORC_SEEN(r) (limit ? (limit[r] + 1 < 0 ? 0 : (limit[r] + 1 < N ? limit[r] + 1 : N)) : N)
     for (int r = 0; r < R; ++r) {
         const double* l = logit + (size_t)r * N;
+        const int n = ORC_SEEN(r);
         double m = -INFINITY;
-        for (int j = 0; j < N; ++j)
+        for (int j = 0; j < n; ++j)
             if (l[j] > m) m = l[j];
         double z = 0.0;
-        for (int j = 0; j < N; ++j) z += exp(l[j] - m);
-        lse[r] = (N > 0) ? m + log(z) : -INFINITY;
+        for (int j = 0; j < n; ++j) z += exp(l[j] - m);
+        lse[r] = (n > 0) ? m + log(z) : -INFINITY;
     }
     for (int j = 0; j < N; ++j) {
-        double best = -INFINITY;
+        double best = -INFINITY, sum = 0.0;
         for (int r = 0; r < R; ++r) {
-            double v = logit[(size_t)r * N + j] - lse[r];
+            if (j >= ORC_SEEN(r)) continue;
+            const double v = logit[(size_t)r * N + j] - lse[r];
             if (v > best) best = v;
+            sum += exp(v);
         }
-        s[j] = best;
+        s[j] = agg ? log(sum / (double)R) : best;
     }
+#undef ORC_SEEN
     free(logit);
     free(krow);
     return 0;
 }
 
+int orc_score(int R, int N, int D, const double* Y, const void* Khead, int dtype, double scale,
+              double* lse, double* s) {
+    return orc_score_ex(R, N, D, Y, Khead, dtype, scale, 0, NULL, lse, s);
+}
+
 /* Score one kv-head from raw inputs: rows (a2) then (a3).  lse_slot is
  * indexed by slot (C beacon slots, then G*W recent rows); empty beacon
  * slots read -inf. */
-int orc_score_head(int dtype, int D, int N, int C, int G, int W, const void* Khead,
-                   const void* qwin_block, const float* beacons, const int32_t* counts,
-                   const float* cos_t, const float* sin_t, float scale, double* lse_slot,
-                   double* s) {
+/* causal = 1 limits recent query w of each query head (slot C + g*W + w,
+ * the W recent queries taken oldest first, the newest at the current step
+ * N - 1) to the keys up to its own position N - W + w; beacon rows see all
+ * keys. */
+int orc_score_head_ex(int dtype, int D, int N, int C, int G, int W, const void* Khead,
+                      const void* qwin_block, const float* beacons, const int32_t* counts,
+                      const float* cos_t, const float* sin_t, float scale, int agg, int causal,
+                      double* lse_slot, double* s) {
     int Rmax = C + G * W;
     double* Y = (double*)malloc(sizeof(double) * (size_t)(Rmax > 0 ? Rmax : 1) * D);
     int32_t* slot = (int32_t*)malloc(sizeof(int32_t) * (size_t)(Rmax > 0 ? Rmax : 1));
+    int32_t* limit = (int32_t*)malloc(sizeof(int32_t) * (size_t)(Rmax > 0 ? Rmax : 1));
     double* lse = (double*)malloc(sizeof(double) * (size_t)(Rmax > 0 ? Rmax : 1));
-    if (!Y || !slot || !lse) {
+    if (!Y || !slot || !limit || !lse) {
         free(Y);
         free(slot);
+        free(limit);
         free(lse);
         return -2;
     }
     int R = orc_assemble_rows(dtype, D, C, G, W, beacons, counts, cos_t, sin_t, qwin_block, Y, slot);
+    for (int r = 0; r < R; ++r) limit[r] = (slot[r] < C) ? N - 1 : N - W + (slot[r] - C) % W;
     double sc = (scale == 0.0f) ? (double)(float)(1.0 / sqrt((double)D)) : (double)scale;
-    int rc = orc_score(R, N, D, Y, Khead, dtype, sc, lse, s);
+    int rc = orc_score_ex(R, N, D, Y, Khead, dtype, sc, agg, causal ? limit : NULL, lse, s);
     for (int i = 0; i < Rmax; ++i) lse_slot[i] = -INFINITY;
     for (int r = 0; r < R; ++r) lse_slot[slot[r]] = lse[r];
     free(Y);
     free(slot);
+    free(limit);
     free(lse);
     return rc;
+}
+
+int orc_score_head(int dtype, int D, int N, int C, int G, int W, const void* Khead,
+                   const void* qwin_block, const float* beacons, const int32_t* counts,
+                   const float* cos_t, const float* sin_t, float scale, double* lse_slot,
+                   double* s) {
+    return orc_score_head_ex(dtype, D, N, C, G, W, Khead, qwin_block, beacons, counts, cos_t, sin_t, scale, 0,
+                             0, lse_slot, s);
 }
 
 /* ---- (a4) selection -------------------------------------------------------
@@ -363,17 +402,25 @@ int orc_compact(int esize, int D, int n_keep, const int32_t* kept, void* Khead, 
 
 /* ---- (a6) the whole eviction of one kv-head: (a2) -> (a3) -> (a4) -> (a5).
  * Returns the number of rows kept (or a negative error). */
-int orc_evict_head(int dtype, int D, int N, int C, int G, int W, int budget, int n_prefix,
-                   void* Khead, void* Vhead, const void* qwin_block, const float* beacons,
-                   const int32_t* counts, const float* cos_t, const float* sin_t, float scale,
-                   double* lse_slot, double* s, int32_t* kept) {
-    int rc = orc_score_head(dtype, D, N, C, G, W, Khead, qwin_block, beacons, counts, cos_t,
-                            sin_t, scale, lse_slot, s);
+int orc_evict_head_ex(int dtype, int D, int N, int C, int G, int W, int budget, int n_prefix,
+                      void* Khead, void* Vhead, const void* qwin_block, const float* beacons,
+                      const int32_t* counts, const float* cos_t, const float* sin_t, float scale, int agg,
+                      int causal, double* lse_slot, double* s, int32_t* kept) {
+    int rc = orc_score_head_ex(dtype, D, N, C, G, W, Khead, qwin_block, beacons, counts, cos_t,
+                               sin_t, scale, agg, causal, lse_slot, s);
     if (rc) return rc;
     int n = orc_topk(N, s, budget, W, n_prefix, kept);
     if (n < 0) return n;
     rc = orc_compact(dtype == ORC_BF16 ? 2 : 4, D, n, kept, Khead, Vhead);
     return rc ? rc : n;
+}
+
+int orc_evict_head(int dtype, int D, int N, int C, int G, int W, int budget, int n_prefix,
+                   void* Khead, void* Vhead, const void* qwin_block, const float* beacons,
+                   const int32_t* counts, const float* cos_t, const float* sin_t, float scale,
+                   double* lse_slot, double* s, int32_t* kept) {
+    return orc_evict_head_ex(dtype, D, N, C, G, W, budget, n_prefix, Khead, Vhead, qwin_block, beacons, counts,
+                             cos_t, sin_t, scale, 0, 0, lse_slot, s, kept);
 }
 
 /* ---- farthest point sampling over pre-RoPE queries ----------------------
