@@ -143,6 +143,28 @@ bkv_status bkv_score(const bkv_dims* d, const void* K, const void* q_win, const 
                      float scale, float* scores, float* row_lse, void* ws, size_t ws_bytes,
                      hipStream_t stream);
 
+/* Scoring options (bit flags) for bkv_score_ex and bkv_evict_ex.
+ *   BKV_SCORE_MEAN    the mean form of Eq. (6) instead of the max: the
+ *                     paper's Table 2 ablation.  scores[j] =
+ *                     ln((1/R) sum_r exp(l_rj - lse_r)) <= 0, R the number
+ *                     of rows (occupied beacon slots plus G*W).
+ *   BKV_SCORE_CAUSAL  the W recent queries of each query head are taken
+ *                     oldest first, the last one at the current step, and
+ *                     recent query w sees only the keys j <= N - W + w: its
+ *                     lse runs over those keys and its weight on later keys
+ *                     is 0 (a causal attention row).  Beacon rows see every
+ *                     key.  A row that sees no key has row_lse -inf and
+ *                     weight 0; a key that no row sees scores -inf. */
+#define BKV_SCORE_MEAN 1
+#define BKV_SCORE_CAUSAL 2
+
+/* bkv_score with options; flags 0 is bkv_score.  Unknown flag bits are
+ * BKV_ERR_INVALID. */
+bkv_status bkv_score_ex(const bkv_dims* d, int32_t flags, const void* K, const void* q_win,
+                        const float* beacons, const int32_t* counts, const float* rope_cos,
+                        const float* rope_sin, float scale, float* scores, float* row_lse, void* ws,
+                        size_t ws_bytes, hipStream_t stream);
+
 /* (a4) Selection.  If N <= budget, kept = 0..N-1.  Otherwise the first
  * n_prefix and the last W tokens are always kept and the remaining
  * budget - n_prefix - W places go to the other tokens of highest score,
@@ -209,6 +231,12 @@ bkv_status bkv_fps(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, co
 bkv_status bkv_fps_gather(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* src,
                           int32_t src_rows, void* dst, int32_t dst_dtype, int32_t dst_rows, int32_t* picks,
                           int32_t* counts, hipStream_t stream);
+
+/* bkv_evict with scoring options (see bkv_score_ex); flags 0 is bkv_evict. */
+bkv_status bkv_evict_ex(const bkv_dims* d, int32_t flags, void* K, void* V, const void* q_win,
+                        const float* beacons, const int32_t* counts, const float* rope_cos,
+                        const float* rope_sin, float scale, int32_t* kept, float* scores, float* row_lse,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* bkv_status_string(bkv_status s);

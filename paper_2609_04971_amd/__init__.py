@@ -24,7 +24,9 @@ OP_BEACON_UPDATE, OP_SCORE, OP_TOPK, OP_COMPACT, OP_EVICT = range(5)
 
 EXPORTS = ("bkv_validate", "bkv_workspace_bytes", "bkv_workspace_init", "bkv_device_status",
            "bkv_beacon_update", "bkv_score", "bkv_topk", "bkv_compact", "bkv_evict",
-           "bkv_fps", "bkv_fps_gather", "bkv_status_string", "bkv_abi_version")
+           "bkv_score_ex", "bkv_evict_ex", "bkv_fps", "bkv_fps_gather", "bkv_status_string",
+           "bkv_abi_version")
+SCORE_MEAN, SCORE_CAUSAL = 1, 2
 
 
 class Dims(ctypes.Structure):
@@ -76,6 +78,8 @@ _SIGS = {
     "bkv_topk": ([_D, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_compact": ([_D, _P, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_evict": ([_D, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_score_ex": ([_D, _I, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_evict_ex": ([_D, _I, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_fps": ([_I] * 5 + [_P, _I, _P, _P], ctypes.c_int),
     "bkv_fps_gather": ([_I] * 5 + [_P, _I, _P, _I, _I, _P, _P, _P], ctypes.c_int),
     "bkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
@@ -196,20 +200,25 @@ def _rope(rope_cos, rope_sin, d):
             _ptr(rope_sin, (d.D // 2,), torch.float32, "rope_sin", optional=True))
 
 
+def _flags(mean, causal):
+    return (SCORE_MEAN if mean else 0) | (SCORE_CAUSAL if causal else 0)
+
+
 def score(d: Dims, K, q_win, beacons, counts, scores, ws, row_lse=None, rope_cos=None, rope_sin=None,
-          scale: float = 0.0):
-    """(a2)+(a3): scores [B,Hkv,N] fp32 (and row_lse [B,Hkv,C+G*W]) written."""
+          scale: float = 0.0, mean: bool = False, causal: bool = False):
+    """(a2)+(a3): scores [B,Hkv,N] fp32 (and row_lse [B,Hkv,C+G*W]) written.
+    mean / causal select the scoring options of bkv_score_ex."""
     rc, rs = _rope(rope_cos, rope_sin, d)
     wp, wn = _ws(ws)
-    st = lib().bkv_score(
-        ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+    st = lib().bkv_score_ex(
+        ctypes.byref(d), _flags(mean, causal), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
         _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),
         _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
         _ptr(counts, (d.B, d.Hkv, d.C), torch.int32, "counts"), rc, rs, float(scale),
         _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores"),
         _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True), wp, wn,
         _stream())
-    _check(st, "bkv_score")
+    _check(st, "bkv_score_ex")
 
 
 def topk(d: Dims, scores, kept, ws=None):
@@ -230,12 +239,13 @@ def compact(d: Dims, K, V, kept, ws):
 
 
 def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row_lse=None, rope_cos=None,
-          rope_sin=None, scale: float = 0.0):
-    """(a6): score -> select -> compact one layer in place."""
+          rope_sin=None, scale: float = 0.0, mean: bool = False, causal: bool = False):
+    """(a6): score -> select -> compact one layer in place (scoring options
+    as in score)."""
     rc, rs = _rope(rope_cos, rope_sin, d)
     wp, wn = _ws(ws)
-    st = lib().bkv_evict(
-        ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+    st = lib().bkv_evict_ex(
+        ctypes.byref(d), _flags(mean, causal), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
         _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
         _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),
         _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
@@ -244,7 +254,7 @@ def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row
         _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores", optional=True),
         _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True), wp, wn,
         _stream())
-    _check(st, "bkv_evict")
+    _check(st, "bkv_evict_ex")
 
 
 # ---- Continual FPS -------------------------------------------------------------

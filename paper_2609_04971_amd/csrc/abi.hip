@@ -168,6 +168,14 @@ static bkv_status check_score_args(const bkv_dims* d, const void* K, const void*
 bkv_status bkv_score(const bkv_dims* d, const void* K, const void* q_win, const float* beacons,
                      const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
                      float* scores, float* row_lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+    return bkv_score_ex(d, 0, K, q_win, beacons, counts, rope_cos, rope_sin, scale, scores, row_lse, ws, ws_bytes,
+                        stream);
+}
+
+bkv_status bkv_score_ex(const bkv_dims* d, int32_t flags, const void* K, const void* q_win, const float* beacons,
+                        const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
+                        float* scores, float* row_lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (flags & ~(BKV_SCORE_MEAN | BKV_SCORE_CAUSAL)) return BKV_ERR_INVALID;
     bkv_status st = bkv_validate(d, BKV_OP_SCORE);
     if (st != BKV_OK) return st;
     if (empty_batch(d) || d->N == 0) return BKV_OK;
@@ -176,7 +184,7 @@ bkv_status bkv_score(const bkv_dims* d, const void* K, const void* q_win, const 
     if (!scores) return BKV_ERR_INVALID;
     const WsLayout L = ws_layout(*d);
     if (!ws || ws_bytes < L.score_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
-    return map_hip(launch_score(*d, L, K, q_win, beacons, counts, rope_cos, rope_sin, scale, scores, row_lse, ws,
+    return map_hip(launch_score(*d, L, flags, K, q_win, beacons, counts, rope_cos, rope_sin, scale, scores, row_lse, ws,
                                 stream));
 }
 
@@ -207,6 +215,15 @@ bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, con
                      const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
                      int32_t* kept, float* scores, float* row_lse, void* ws, size_t ws_bytes,
                      hipStream_t stream) {
+    return bkv_evict_ex(d, 0, K, V, q_win, beacons, counts, rope_cos, rope_sin, scale, kept, scores, row_lse, ws,
+                        ws_bytes, stream);
+}
+
+bkv_status bkv_evict_ex(const bkv_dims* d, int32_t flags, void* K, void* V, const void* q_win, const float* beacons,
+                        const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
+                        int32_t* kept, float* scores, float* row_lse, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+    if (flags & ~(BKV_SCORE_MEAN | BKV_SCORE_CAUSAL)) return BKV_ERR_INVALID;
     bkv_status st = bkv_validate(d, BKV_OP_EVICT);
     if (st != BKV_OK) return st;
     if (empty_batch(d) || d->N == 0) return BKV_OK;
@@ -218,7 +235,8 @@ bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, con
     char* w = static_cast<char*>(ws);
     float* sc = scores ? scores : reinterpret_cast<float*>(w + L.scores);
     int32_t* kp = kept ? kept : reinterpret_cast<int32_t*>(w + L.kept);
-    hipError_t e = launch_score(*d, L, K, q_win, beacons, counts, rope_cos, rope_sin, scale, sc, row_lse, ws, stream);
+    hipError_t e =
+        launch_score(*d, L, flags, K, q_win, beacons, counts, rope_cos, rope_sin, scale, sc, row_lse, ws, stream);
     if (e != hipSuccess) return BKV_ERR_HIP;
     e = launch_topk(*d, sc, kp, stream);
     if (e != hipSuccess) return BKV_ERR_HIP;

@@ -71,7 +71,7 @@ hipError_t launch_ws_init(void* ws, size_t ctl_bytes, int P, int budget, hipStre
 hipError_t launch_beacon_update(const bkv_dims& d, const void* q_new, int T, float* beacons,
                                 int32_t* counts, int32_t* assign, hipStream_t s);
 
-hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, const void* q_win,
+hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const void* K, const void* q_win,
                         const float* beacons, const int32_t* counts, const float* rope_cos,
                         const float* rope_sin, float scale, float* scores, float* row_lse,
                         void* ws, hipStream_t s);

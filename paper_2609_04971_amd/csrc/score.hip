@@ -86,7 +86,26 @@ struct Args {
     int R_pad_max, nch, key_chunk, lag, total;
     float s2;     // scale * log2(e)
     float s2ln2;  // s2 * ln(2): log2-units-of-raw-dot -> natural log
+    int mean;     // aggregate by the mean over rows (else the max)
+    int causal;   // recent row w sees keys up to N - W + w only
 };
+
+// Which (key, row) pairs enter the scores: keys at or past N never do, and
+// with the causal option recent row w of a query head (rows nact..R-1 of
+// the head, w = (row - nact) % W, oldest first) sees keys up to its own
+// position N - W + w only.  Beacon rows and padding rows see every key.
+struct KeyMask {
+    int N, W, nact, R, causal;
+    __device__ __forceinline__ int limit(int row) const {  // last key the row sees
+        return (causal && row >= nact && row < R) ? N - W + (row - nact) % W : N - 1;
+    }
+    // keys below this are seen by every row
+    __device__ __forceinline__ int all_see_below() const { return causal ? min(N, N - W + 1) : N; }
+};
+
+__device__ __forceinline__ KeyMask key_mask(const Args& a, int nact) {
+    return KeyMask{a.N, a.W, nact, nact + a.G * a.W, a.causal};
+}
 
 // Per-lane operand: NV 16-byte vectors of one row.  Vector v of lane group
 // g (lane >> 4) holds bytes [64 v + 16 g, 64 v + 16 g + 16) of the row, so
@@ -257,11 +276,13 @@ __device__ void fold_and_publish(const Args& a, int h, const int* act, int nact,
                     if (c0 + u < a.nch) merge_mz(mm, zz, pm[u], pz[u]);
             }
         }
-        const float l2 = (r < R) ? mm + log2f(zz) : INFINITY;  // padding rows never win
+        // padding rows, and rows that see no key, never contribute: +inf
+        // seeds their final pass at -inf
+        const float l2 = (r < R && zz > 0.f) ? mm + log2f(zz) : INFINITY;
         dev::st_coherent(a.lse2 + (size_t)h * a.R_pad_max + r, l2);
         if (a.row_lse && r < R) {
             const int slot = (r < nact) ? act[r] : a.C + (r - nact);
-            a.row_lse[(size_t)h * (a.C + a.G * a.W) + slot] = l2 * 0.69314718055994531f;
+            a.row_lse[(size_t)h * (a.C + a.G * a.W) + slot] = (zz > 0.f) ? l2 * 0.69314718055994531f : -INFINITY;
         }
     }
     if (a.row_lse) {  // empty beacon slots have no row
@@ -299,9 +320,9 @@ __device__ __forceinline__ bool await_lse(const Args& a, int h, int* s_flag) {
 //
 // Wave w takes keys [kw, kw + 64*KGN) in groups of 64 (four 16-key tiles).
 // MFMA rows are keys and columns observation rows, so a lane owns one row
-// (lane & 15 within the tile) and 16 keys of each group.  Keys at or past N
-// enter with the accumulator seeded at -inf, so they add exp2(-inf) = 0 and
-// need no per-element masking.
+// (lane & 15 within the tile) and 16 keys of each group.  (key, row) pairs
+// outside the mask (keys at or past N, the causal window) enter with the
+// accumulator seeded at -inf, so they add exp2(-inf) = 0.
 template <typename T, int D, int KGN>
 __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int* s_flag) {
     constexpr int RG = Tr<T>::RG, LD = D + Tr<T>::PAD, RTM = RG / 16;
@@ -317,6 +338,7 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     const int N = a.N;
     const float s2 = a.s2;
     const size_t pbase = ((size_t)h * a.nch + chunk) * a.R_pad_max;
+    const KeyMask mk = key_mask(a, nact);
 
     for (int r0 = 0; r0 < Rp; r0 += RG) {
         const int nr = min(RG, Rp - r0), RT = nr / 16;
@@ -335,20 +357,19 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             const int kb = kw + kg * 64;
             Op<T, D> kop[4];
             load_group<T, D>(kop, Kh, kb, N, c16, g);
-            f32x4 seed[4];  // 0 for keys below N, -inf past it
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) seed[t][v] = (kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
+            const bool masked = kb + 64 > mk.all_see_below();  // some (key, row) pair is out
 #pragma unroll
             for (int rt = 0; rt < RTM; ++rt) {
                 if (rt < RT) {
                     Op<T, D> yop;
                     load_row_tile<T, D>(yop, sm.y + (rt * 16 + c16) * LD, g);
+                    // 0, or -inf for keys this lane's row does not see
+                    const int lim = masked ? mk.limit(r0 + rt * 16 + c16) : N;
                     f32x4 acc[4];
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
-                        acc[t] = seed[t];
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) acc[t][v] = (kb + t * 16 + 4 * g + v <= lim) ? 0.f : -INFINITY;
                         mma(acc[t], kop[t], yop);  // rows = keys, columns = observation rows
                     }
                     float gm = fmaxf(fmaxf(acc[0][0], acc[0][1]), fmaxf(acc[0][2], acc[0][3]));
@@ -392,12 +413,13 @@ __device__ void stats_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     if (count_stats(a, h, s_flag)) fold_and_publish(a, h, sm.act, nact, a.hctl + (size_t)h * kHcWords);
 }
 
-// ---- F(h, chunk): final max-aggregated scores over one key chunk ----------
+// ---- F(h, chunk): final scores over one key chunk ----------------------
 //
 // MFMA rows are observation rows and columns keys; the accumulator starts at
 // -lse2_r / s2, so each output is (l_rj - lse_r) / (s2 ln 2) and a key's
-// score is the max down its column.  Per-key maxima collect in LDS (across
-// row groups) and are written out coalesced at the end.
+// score is the max down its column (or, for the mean, the log of the mean
+// of the weights exp2(s2 * output)).  Per-key maxima (sums) collect in LDS
+// across row groups and are written out coalesced at the end.
 template <typename T, int D, int KGN>
 __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int* s_flag) {
     constexpr int RG = Tr<T>::RG, LD = D + Tr<T>::PAD, RTM = RG / 16;
@@ -412,8 +434,10 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     const int k0 = chunk * KC;
     const int kw = k0 + wave * 64 * KGN;
     const int N = a.N;
-    const float inv_s2 = 1.0f / a.s2;
-    for (int i = tid; i < KC; i += kThreads) sm.best[i] = -INFINITY;
+    const float inv_s2 = 1.0f / a.s2, s2 = a.s2;
+    const KeyMask mk = key_mask(a, sm.nact);
+    const bool mean = a.mean != 0;
+    for (int i = tid; i < KC; i += kThreads) sm.best[i] = mean ? 0.f : -INFINITY;
     const int ngroups = max(0, min(KGN, (N - kw + 63) / 64));
 
     for (int r0 = 0; r0 < Rp; r0 += RG) {
@@ -428,7 +452,10 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             const int kb = kw + kg * 64;
             Op<T, D> kop[4];
             load_group<T, D>(kop, Kh, kb, N, c16, g);
-            float best[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            const bool masked = kb + 64 > mk.all_see_below();
+            float best[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) best[t] = mean ? 0.f : -INFINITY;
 #pragma unroll
             for (int rt = 0; rt < RTM; ++rt) {
                 if (rt < RT) {
@@ -438,25 +465,43 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
                         f32x4 acc = c0;
+                        if (masked) {  // (key, row) pairs outside the mask start at -inf
+                            const int key = kb + t * 16 + c16;
+#pragma unroll
+                            for (int v = 0; v < 4; ++v)
+                                if (key > mk.limit(r0 + rt * 16 + 4 * g + v)) acc[v] = -INFINITY;
+                        }
                         mma(acc, yop, kop[t]);  // rows = observation rows, columns = keys
-                        best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
+                        if (mean)
+                            best[t] += (fast_exp2(acc[0] * s2) + fast_exp2(acc[1] * s2)) +
+                                       (fast_exp2(acc[2] * s2) + fast_exp2(acc[3] * s2));
+                        else
+                            best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
                     }
                 }
             }
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 float b = best[t];
-                b = fmaxf(b, dev::shfl_xor_f(b, 16));
-                b = fmaxf(b, dev::shfl_xor_f(b, 32));
                 float* slot = sm.best + (kb - k0) + t * 16 + c16;  // this wave's own keys
-                if (g == t) *slot = fmaxf(*slot, b);
+                if (mean) {
+                    b += dev::shfl_xor_f(b, 16);
+                    b += dev::shfl_xor_f(b, 32);
+                    if (g == t) *slot += b;
+                } else {
+                    b = fmaxf(b, dev::shfl_xor_f(b, 16));
+                    b = fmaxf(b, dev::shfl_xor_f(b, 32));
+                    if (g == t) *slot = fmaxf(*slot, b);
+                }
             }
         }
     }
     __syncthreads();
     float* out = a.scores + (size_t)h * N;
+    const float log2R = log2f((float)R);
     for (int i = tid; i < KC; i += kThreads)
-        if (k0 + i < N) out[k0 + i] = sm.best[i] * a.s2ln2;
+        if (k0 + i < N)
+            out[k0 + i] = mean ? (log2f(sm.best[i]) - log2R) * 0.69314718055994531f : sm.best[i] * a.s2ln2;
 }
 
 // Workgroup -> head.  The grid lists, for s = 0, 1, ..., nch workgroups of
@@ -581,7 +626,14 @@ struct alignas(16) FastSmem {
         } red;                  // S items: per-wave row statistics
         float nlse[kFRT * 16];  // F items: -lse of each row (raw-dot units)
     } v;
+    int lim[kFRT * 16];         // last key each row sees (KeyMask::limit)
 };
+
+// Each row's key limit into LDS, for the groups that mask (key, row) pairs.
+template <int RT>
+__device__ __forceinline__ void fill_limits(const KeyMask& mk, int* lim) {
+    for (int r = threadIdx.x; r < RT * 16; r += kThreads) lim[r] = mk.limit(r);
+}
 
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
 template <int N>
@@ -646,10 +698,14 @@ __device__ __forceinline__ void issue_group(const uint16_t* Kh, int kb, int N, u
     using KS = KeyStage<D>;
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)(Kh + (size_t)kb * D), (short)0, min(N - kb, kFKG) * D * 2, 0x00020000);
+    // the offsets are recomputed at every issue: hoisted out of the key
+    // loop they would hold NI registers for the whole item
+    int l = lane;
+    asm volatile("" : "+v"(l));
 #pragma unroll
     for (int j = 0; j < KS::NI; ++j)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + j * 512),
-                                                 16, group_offset<D>(j, lane), 0, 0, 0);
+                                                 16, group_offset<D>(j, l), 0, 0, 0);
 #endif
 }
 
@@ -666,8 +722,9 @@ __device__ __forceinline__ void read_key_tile(Op<uint16_t, D>& op, const uint16_
 }
 
 // Running (max, sum) of one S item over one staged group of 32 keys.
-// Keys at or past N (only in a head's last group, TAIL) enter with the
-// accumulator seeded at -inf, so they add exp2(-inf) = 0.
+// In groups holding keys some row may not see (TAIL: keys at or past N, or
+// the causal window) those (key, row) pairs enter with the accumulator
+// seeded at -inf, so they add exp2(-inf) = 0.
 //
 // Software-pipelined by one row tile: the MFMAs of tile rt + 1 are issued
 // in the same scheduling region as the exp/max work on tile rt and
@@ -676,17 +733,18 @@ __device__ __forceinline__ void read_key_tile(Op<uint16_t, D>& op, const uint16_
 // two tiles of accumulators are live at a time; hoisting more would spill
 // the registers that hold the rows.
 template <int D, int RT, bool TAIL>
-__device__ __forceinline__ void stats_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr, float s2,
-                                            float* m, float* z, int c16, int g) {
+__device__ __forceinline__ void stats_group(const uint16_t* st, int kb, const int* lim, const Op<uint16_t, D>* yr,
+                                            float s2, float* m, float* z, int c16, int g) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
     f32x4 acc[2][2];
     auto issue = [&](int rt, f32x4* a) {
+        const int l = TAIL ? lim[rt * 16 + c16] : 0;  // this lane's row
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) a[t][v] = (!TAIL || kb + t * 16 + 4 * g + v < N) ? 0.f : -INFINITY;
+            for (int v = 0; v < 4; ++v) a[t][v] = (!TAIL || kb + t * 16 + 4 * g + v <= l) ? 0.f : -INFINITY;
             mma(a[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
         }
     };
@@ -715,17 +773,20 @@ __device__ __forceinline__ void stats_group(const uint16_t* st, int kb, int N, c
 }
 
 // Scores of one F item's staged group of 32 keys: per key the maximum over
-// rows, written straight out (64 contiguous bytes per 16-key tile).
+// rows (or the log of the mean weight), written straight out (64 contiguous
+// bytes per 16-key tile).  TAIL groups mask (key, row) pairs as in S.
 // Pipelined like stats_group; each tile's -lse seed is read from LDS two
 // tiles ahead (re-read every group through an offset the compiler cannot
 // hoist: kept for the whole item these would hold 4 * RT registers).
-template <int D, int RT>
-__device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, const Op<uint16_t, D>* yr,
-                                            const float* nlse, float* out, float s2ln2, int c16, int g) {
+template <int D, int RT, bool MEAN, bool TAIL>
+__device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, const int* lim, const Op<uint16_t, D>* yr,
+                                            const float* nlse, float* out, float s2, float log2R, int c16, int g) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
-    float best[2] = {-INFINITY, -INFINITY};
+    // per key of this lane: max of (l - lse) / s2 over rows, or the sum of
+    // the weights exp2(s2 * acc) for the mean
+    float best[2] = {MEAN ? 0.f : -INFINITY, MEAN ? 0.f : -INFINITY};
     f32x4 acc[2][2];
     f32x4 cn[2];
     auto load_c = [&](int rt) {
@@ -733,6 +794,37 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
         asm volatile("" : "+v"(off));
         return *reinterpret_cast<const f32x4*>(nlse + off);
     };
+    auto accumulate = [&](const f32x4* a) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            if constexpr (MEAN)
+                best[t] += (fast_exp2(a[t][0] * s2) + fast_exp2(a[t][1] * s2)) +
+                           (fast_exp2(a[t][2] * s2) + fast_exp2(a[t][3] * s2));
+            else
+                best[t] = fmaxf(best[t], fmaxf(fmaxf(a[t][0], a[t][1]), fmaxf(a[t][2], a[t][3])));
+        }
+    };
+    if constexpr (TAIL) {
+        // a head's last groups only: one row tile at a time, (key, row)
+        // pairs outside the mask seeded at -inf
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const f32x4 c0 = load_c(rt);
+            const int4 l4 = *reinterpret_cast<const int4*>(lim + rt * 16 + 4 * g);
+            f32x4* a = acc[0];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int key = kb + t * 16 + c16;
+                a[t][0] = key > l4.x ? -INFINITY : c0[0];
+                a[t][1] = key > l4.y ? -INFINITY : c0[1];
+                a[t][2] = key > l4.z ? -INFINITY : c0[2];
+                a[t][3] = key > l4.w ? -INFINITY : c0[3];
+                mma(a[t], yr[rt], kop[t]);  // rows = observation rows, columns = keys
+            }
+            accumulate(a);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
     auto issue = [&](int rt, f32x4* a, const f32x4& c0) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -746,22 +838,28 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
     dev::static_for<RT>([&](auto rt) {
         if constexpr (rt + 2 < RT) cn[rt & 1] = load_c(rt + 2);
         if constexpr (rt + 1 < RT) issue(rt + 1, acc[(rt + 1) & 1], cn[(rt + 1) & 1]);
-        f32x4* a = acc[rt & 1];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) best[t] = fmaxf(best[t], fmaxf(fmaxf(a[t][0], a[t][1]), fmaxf(a[t][2], a[t][3])));
+        accumulate(acc[rt & 1]);
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // one VALU
+            __builtin_amdgcn_sched_group_barrier(0x002, MEAN ? 4 : 1, 0);  // VALU
         }
         __builtin_amdgcn_sched_barrier(0);
     });
+    }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
         float b = best[t];
-        b = fmaxf(b, dev::shfl_xor_f(b, 16));
-        b = fmaxf(b, dev::shfl_xor_f(b, 32));
-        if (g == t && kb + t * 16 + c16 < N) out[kb + t * 16 + c16] = b * s2ln2;
+        if constexpr (MEAN) {
+            b += dev::shfl_xor_f(b, 16);
+            b += dev::shfl_xor_f(b, 32);
+            b = (log2f(b) - log2R) * 0.69314718055994531f;  // ln of the mean weight
+        } else {
+            b = fmaxf(b, dev::shfl_xor_f(b, 16));
+            b = fmaxf(b, dev::shfl_xor_f(b, 32));
+            b *= s2 * 0.69314718055994531f;
+        }
+        if (g == t && kb + t * 16 + c16 < N) out[kb + t * 16 + c16] = b;
     }
 }
 
@@ -791,6 +889,10 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageB
     if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
     if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
     const float s2 = a.s2;
+    const KeyMask mk = key_mask(a, a.rmeta[(size_t)h * kMetaWords]);
+    const int clear_below = mk.all_see_below();
+    fill_limits<RT>(mk, sm.lim);
+    __syncthreads();
     float m[RT], z[RT];
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
@@ -801,17 +903,17 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageB
     for (int kg = 0; kg < ngroups; kg += 2) {
         const int kb = kw + kg * kFKG;
         wait_group<D>(kg + 1 < ngroups);
-        if (kb + kFKG <= N)
-            stats_group<D, RT, false>(stA, kb, N, yr, s2, m, z, c16, g);
+        if (kb + kFKG <= clear_below)
+            stats_group<D, RT, false>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
         else
-            stats_group<D, RT, true>(stA, kb, N, yr, s2, m, z, c16, g);
+            stats_group<D, RT, true>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
         if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
         if (kg + 1 < ngroups) {
             wait_group<D>(kg + 2 < ngroups);
-            if (kb + 2 * kFKG <= N)
-                stats_group<D, RT, false>(stB, kb + kFKG, N, yr, s2, m, z, c16, g);
+            if (kb + 2 * kFKG <= clear_below)
+                stats_group<D, RT, false>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
             else
-                stats_group<D, RT, true>(stB, kb + kFKG, N, yr, s2, m, z, c16, g);
+                stats_group<D, RT, true>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
             if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
         }
     }
@@ -840,6 +942,32 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageB
     }
 }
 
+// The F item's key loop (both stages already in flight).
+template <int D, int RT, bool MEAN>
+__device__ __forceinline__ void final_loop(const uint16_t* Kh, int kw, int ngroups, int N, int clear_below,
+                                           const int* lim, uint16_t* stA, uint16_t* stB, const Op<uint16_t, D>* yr,
+                                           const float* nlse, float* out, float s2, float log2R, int lane, int c16,
+                                           int g) {
+    auto body = [&](const uint16_t* st, int kb) {
+        if (kb + kFKG <= clear_below)
+            final_group<D, RT, MEAN, false>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g);
+        else
+            final_group<D, RT, MEAN, true>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g);
+    };
+#pragma unroll 1
+    for (int kg = 0; kg < ngroups; kg += 2) {
+        const int kb = kw + kg * kFKG;
+        wait_group<D>(kg + 1 < ngroups);
+        body(stA, kb);
+        if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
+        if (kg + 1 < ngroups) {
+            wait_group<D>(kg + 2 < ngroups);
+            body(stB, kb + kFKG);
+            if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
+        }
+    }
+}
+
 template <int D, int RT>
 __device__ void fast_final(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
                            const Op<uint16_t, D>* yr, int* s_flag) {
@@ -861,23 +989,19 @@ __device__ void fast_final(const Args& a, int h, int chunk, FastSmem& sm, StageB
         return;
     }
     const float inv_s2 = 1.0f / a.s2;
+    const KeyMask mk = key_mask(a, a.rmeta[(size_t)h * kMetaWords]);
     for (int r = tid; r < RT * 16; r += kThreads)
         sm.v.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r) * inv_s2;
+    fill_limits<RT>(mk, sm.lim);
     __syncthreads();
     float* out = a.scores + (size_t)h * N;
-    const float s2ln2 = a.s2ln2;
-#pragma unroll 1
-    for (int kg = 0; kg < ngroups; kg += 2) {
-        const int kb = kw + kg * kFKG;
-        wait_group<D>(kg + 1 < ngroups);
-        final_group<D, RT>(stA, kb, N, yr, sm.v.nlse, out, s2ln2, c16, g);
-        if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
-        if (kg + 1 < ngroups) {
-            wait_group<D>(kg + 2 < ngroups);
-            final_group<D, RT>(stB, kb + kFKG, N, yr, sm.v.nlse, out, s2ln2, c16, g);
-            if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
-        }
-    }
+    const int clear_below = mk.all_see_below();
+    if (a.mean)
+        final_loop<D, RT, true>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2,
+                                log2f((float)mk.R), lane, c16, g);
+    else
+        final_loop<D, RT, false>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2, 0.f,
+                                 lane, c16, g);
 }
 
 template <int D, int RT>
@@ -932,7 +1056,7 @@ hipError_t launch_t(const Args& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, const void* q_win,
+hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const void* K, const void* q_win,
                         const float* beacons, const int32_t* counts, const float* rope_cos,
                         const float* rope_sin, float scale, float* scores, float* row_lse, void* ws,
                         hipStream_t s) {
@@ -975,6 +1099,8 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, const void* K, con
     const float sc = (scale == 0.0f) ? (float)(1.0 / sqrt((double)d.D)) : scale;
     a.s2 = sc * 1.4426950408889634f;
     a.s2ln2 = a.s2 * 0.69314718055994531f;
+    a.mean = (flags & BKV_SCORE_MEAN) != 0;
+    a.causal = (flags & BKV_SCORE_CAUSAL) != 0;
     const bool bf = d.dtype == BKV_BF16;
     if (bf && L.R_pad_max <= kFRT * 16) {  // all rows fit in registers
         a.rows = reinterpret_cast<uint16_t*>(w + L.rows);

@@ -185,3 +185,21 @@ def test_fps_empty_is_a_no_op():
 ])
 def test_fps_gather_rejects(kw, code):
     assert _gather(**kw) == code
+
+
+def test_score_ex_rejects_unknown_flags_and_keeps_rules():
+    lib = bkv.lib()
+    d = good()
+    r = ctypes.byref(d)
+    assert lib.bkv_score_ex(r, 4, None, None, None, None, None, None, 0.0, None, None, None, 0, None) == \
+        bkv.ERR_INVALID
+    assert lib.bkv_evict_ex(r, 8, None, None, None, None, None, None, None, 0.0, None, None, None, None, 0,
+                            None) == bkv.ERR_INVALID
+    # valid flags, then the same checks as without them
+    for f in (1, 2, 3):
+        assert lib.bkv_score_ex(r, f, None, None, None, None, None, None, 0.0, None, None, None, 0, None) == \
+            bkv.ERR_INVALID
+        assert lib.bkv_score_ex(ctypes.byref(good(D=96)), f, None, None, None, None, None, None, 0.0, None, None,
+                                None, 0, None) == bkv.ERR_SHAPE
+        assert lib.bkv_score_ex(ctypes.byref(good(N=0)), f, None, None, None, None, None, None, 0.0, None, None,
+                                None, 0, None) == bkv.OK
