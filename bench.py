@@ -203,6 +203,8 @@ def main():
         "roofline": roofline,
         "setup_s": round(gen_s, 1),
     }
+    if not args.no_fps:
+        out["score_options"] = score_options_measure(d, layers, scores, ws, score_bytes)
     del layers
     torch.cuda.empty_cache()
     if not args.no_fps:
@@ -210,6 +212,33 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_heads)
     print(json.dumps(out), flush=True)
+
+
+def score_options_measure(d, layers, scores, ws, score_bytes, reps=6):
+    """The score launch with the scoring options of bkv_score_ex (Eq. 6's mean
+    form; causal recent queries), timed with HIP events on the launch stream
+    over `reps` resident layers, outside the eviction step.  Same algorithmic
+    bytes as the max form: K read once, one fp32 score written per row."""
+    import torch
+
+    import paper_2609_04971_amd as bkv
+
+    res = {}
+    for name, mean, causal in (("max", False, False), ("mean", True, False), ("max_causal", False, True),
+                               ("mean_causal", True, True)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            x = layers[i % len(layers)]
+            bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+                      rope_sin=x["rope_sin"], mean=mean, causal=causal)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        gbs = score_bytes / (us * 1e-6) / 1e9
+        res[name] = {"us": round(us, 1), "achieved_GBs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    return res
 
 
 def fps_measure(w, dev, reps=20):
