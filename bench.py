@@ -76,7 +76,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=768,
                     help="(batch, kv-head) pairs in the CPU oracle sample, taken layer by layer")
-    ap.add_argument("--no-fps", action="store_true", help="skip the Continual FPS timings")
+    ap.add_argument("--no-fps", action="store_true", help="skip the Continual FPS and scoring-option timings")
+    ap.add_argument("--no-trace", action="store_true", help="skip the periodic-eviction cycle timing")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -209,6 +210,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_fps:
         out["continual_fps"] = fps_measure(w, dev)
+    if not args.no_trace:
+        out["periodic_eviction"] = trace_measure(w, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_heads)
     print(json.dumps(out), flush=True)
@@ -282,6 +285,70 @@ def fps_measure(w, dev, reps=20):
                      "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                   "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes}}
         del src, dst, picks
+        torch.cuda.empty_cache()
+    return res
+
+
+def trace_measure(w, dev, B_max=4096, pool=16):
+    """One steady-state eviction cycle of the periodic driver (Algorithm 2's
+    phase machine; paper_2609_04971_amd.driver) for all 36 layers of the
+    Qwen3-4B shape at once: the cache starts at B_min = 7/8 B_max after a
+    prefill, then B_max - B_min decode steps run, the last of which evicts
+    every layer back to B_min.  BeaconKV (16 beacon + 16 recent queries per
+    head, Section 5.1) against RPC on the same kernels (32 recent queries,
+    no beacons; Table 1).  Reported: the driver's wall time per step (host
+    plus device, Python included) and the device time of the library calls
+    per cycle from HIP events around each call."""
+    import torch
+
+    from paper_2609_04971_amd import synth
+    from paper_2609_04971_amd.driver import PeriodicEviction
+
+    layers, B, Hq, Hkv, D = w.layers, w.B, w.Hq, w.Hkv, w.D
+    LB = layers * B
+    B_min = 7 * B_max // 8
+    g = torch.Generator(device=dev)
+    g.manual_seed(123)
+    tables = {}
+
+    def table(t):
+        if t not in tables:
+            c, s = synth.rope_table(D, t)
+            tables[t] = (c.to(dev), s.to(dev))
+        return tables[t]
+
+    res = {"config": {"layers": layers, "B": B, "Hq": Hq, "Hkv": Hkv, "D": D, "B_max": B_max, "B_min": B_min,
+                      "steps_per_cycle": B_max - B_min}}
+    for mode, nb, nr in (("beacon", 16, 16), ("rpc", 0, 32)):
+        drv = PeriodicEviction(layers, B, Hq, Hkv, D, B_max, table, n_beacon=max(nb, 1), n_recent=nr, mode=mode,
+                               device=dev, timing=True)
+        Kp = torch.randn(LB, Hkv, B_min, D, generator=g, device=dev, dtype=torch.bfloat16)
+        Vp = torch.randn_like(Kp)
+        qp = synth.query_stream(w.with_(B=LB), B_min, seed=5, device=dev)
+        drv.prefill(Kp, Vp, qp)
+        del Kp, Vp, qp
+        kk = torch.randn(LB, Hkv, pool, D, generator=g, device=dev, dtype=torch.bfloat16)
+        vv = torch.randn_like(kk)
+        qq = synth.query_stream(w.with_(B=LB), pool, seed=6, device=dev)
+        drv.times.clear()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        n = 0
+        while True:
+            i = n % pool
+            n += 1
+            if drv.step(kk[:, :, i], vv[:, :, i], qq[:, :, i], qq[:, :, i]):
+                break
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        per_kind = {}
+        for kind, e0, e1 in drv.times:
+            per_kind[kind] = per_kind.get(kind, 0.0) + e0.elapsed_time(e1) * 1e3
+        dev_us = sum(per_kind.values())
+        res[mode] = {"n_beacon": nb, "n_recent": nr, "steps": n, "wall_us_per_step": round(wall * 1e6 / n, 1),
+                     "library_us_per_cycle": {k: round(v, 1) for k, v in per_kind.items()},
+                     "library_us_per_step": round(dev_us / n, 2)}
+        del drv, kk, vv, qq
         torch.cuda.empty_cache()
     return res
 

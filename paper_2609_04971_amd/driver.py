@@ -40,10 +40,12 @@ import paper_2609_04971_amd as bkv
 class PeriodicEviction:
     def __init__(self, layers: int, B: int, Hq: int, Hkv: int, D: int, B_max: int, rope_table, n_beacon: int = 16,
                  n_recent: int = 16, n_prefix: int = 0, mode: str = "beacon", dtype=torch.bfloat16,
-                 device="cuda", record: bool = False):
+                 device="cuda", record: bool = False, timing: bool = False):
         """rope_table(t) -> (cos, sin), fp32 [D/2] device tensors of the
         model's rotate-half RoPE at absolute position t (the beacons are
-        rotated to the step at which eviction runs)."""
+        rotated to the step at which eviction runs).  record keeps every
+        call's inputs and outputs in `events`; timing brackets every library
+        call with HIP events on the current stream, in `times`."""
         if mode not in ("beacon", "rpc"):
             raise ValueError("mode is 'beacon' or 'rpc'")
         if B_max % 8:
@@ -79,16 +81,28 @@ class PeriodicEviction:
         self.kept = torch.empty(LB, Hkv, self.B_min, dtype=torch.int32, device=dev)
         self.scores = torch.empty(LB, Hkv, B_max, dtype=torch.float32, device=dev)
         self.events = []  # (kind, details) of the calls made, when recording
+        self.timing = timing
+        self.times = []   # (kind, start event, end event), when timing
 
     # ---- helpers --------------------------------------------------------------
     def _log(self, kind, **kw):
         if self.record:
             self.events.append((kind, kw))
 
+    def _call(self, kind, fn):
+        if not self.timing:
+            fn()
+            return
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        self.times.append((kind, e0, e1))
+
     def _compress(self, n: int, why: str):
         picks = torch.empty(self.LB, self.Hq, min(self.nb, n), dtype=torch.int32, device=self.obs.device)
         src = self.obs[:, :, :n].clone() if self.record else None
-        bkv.fps_gather(self.obs, self.nb, n=n, picks=picks)
+        self._call("fps_" + why, lambda: bkv.fps_gather(self.obs, self.nb, n=n, picks=picks))
         self.obs_len = min(self.nb, n)
         self._log("fps", why=why, src=src, picks=picks)
 
@@ -103,7 +117,7 @@ class PeriodicEviction:
         self.L = self.t = T
         if self.mode == "beacon":
             picks = torch.empty(self.LB, self.Hq, min(self.nb, T), dtype=torch.int32, device=K.device)
-            bkv.fps_gather(q_pre, self.nb, dst=self.obs, picks=picks)
+            self._call("fps_prefill", lambda: bkv.fps_gather(q_pre, self.nb, dst=self.obs, picks=picks))
             self.obs_len = min(self.nb, T)
             self._log("fps", why="prefill", src=q_pre.clone() if self.record else None, picks=picks)
 
@@ -125,8 +139,9 @@ class PeriodicEviction:
                 # freeze: the buffer's FPS selection is the beacon set, kept
                 # pre-RoPE in the buffer's first rows and widened for scoring
                 self._compress(self.obs_len, "freeze")
-                bkv.fps_gather(self.obs, nb, n=self.obs_len, dst=self.beacons.view(self.LB, self.Hq, nb, self.D),
-                               counts=self.counts.view(self.LB, self.Hq, nb))
+                self._call("beacon_widen", lambda: bkv.fps_gather(
+                    self.obs, nb, n=self.obs_len, dst=self.beacons.view(self.LB, self.Hq, nb, self.D),
+                    counts=self.counts.view(self.LB, self.Hq, nb)))
                 self.n_rec = 0
         if self.B_max - nr < L <= self.B_max:
             self.recent_rope[:, :, self.n_rec] = q_rope
@@ -140,8 +155,8 @@ class PeriodicEviction:
     def _evict(self):
         rc, rs = self.rope_table(self.t - 1)  # beacons rotated to the current step
         pre = (self.K.clone(), self.V.clone()) if self.record else None
-        bkv.evict(self.dims, self.K, self.V, self.recent_rope, self.beacons, self.counts, self.ws, kept=self.kept,
-                  scores=self.scores, rope_cos=rc, rope_sin=rs)
+        self._call("evict", lambda: bkv.evict(self.dims, self.K, self.V, self.recent_rope, self.beacons, self.counts,
+                                              self.ws, kept=self.kept, scores=self.scores, rope_cos=rc, rope_sin=rs))
         self._log("evict", before=pre, q_win=self.recent_rope.clone() if self.record else None,
                   beacons=self.beacons.clone() if self.record else None,
                   counts=self.counts.clone() if self.record else None, rope=(rc, rs), kept=self.kept.clone(),
