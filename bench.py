@@ -78,6 +78,7 @@ def parse():
                     help="(batch, kv-head) pairs in the CPU oracle sample, taken layer by layer")
     ap.add_argument("--no-fps", action="store_true", help="skip the Continual FPS and scoring-option timings")
     ap.add_argument("--no-trace", action="store_true", help="skip the periodic-eviction cycle timing")
+    ap.add_argument("--no-diag", action="store_true", help="skip the synthetic quality diagnostics")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -212,6 +213,8 @@ def main():
         out["continual_fps"] = fps_measure(w, dev)
     if not args.no_trace:
         out["periodic_eviction"] = trace_measure(w, dev)
+    if not args.no_diag:
+        out["diagnostics"] = diagnostics_measure(w, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_heads)
     print(json.dumps(out), flush=True)
@@ -296,7 +299,8 @@ def trace_measure(w, dev, B_max=4096, pool=16):
     prefill, then B_max - B_min decode steps run, the last of which evicts
     every layer back to B_min.  BeaconKV (16 beacon + 16 recent queries per
     head, Section 5.1) against RPC on the same kernels (32 recent queries,
-    no beacons; Table 1).  Reported: the driver's wall time per step (host
+    no beacons; Table 1) and running-mean beacons (bkv_beacon_update every
+    step, 16 slots per query head).  Reported: the driver's wall time per step (host
     plus device, Python included) and the device time of the library calls
     per cycle from HIP events around each call."""
     import torch
@@ -319,7 +323,7 @@ def trace_measure(w, dev, B_max=4096, pool=16):
 
     res = {"config": {"layers": layers, "B": B, "Hq": Hq, "Hkv": Hkv, "D": D, "B_max": B_max, "B_min": B_min,
                       "steps_per_cycle": B_max - B_min}}
-    for mode, nb, nr in (("beacon", 16, 16), ("rpc", 0, 32)):
+    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("rpc", 0, 32)):
         drv = PeriodicEviction(layers, B, Hq, Hkv, D, B_max, table, n_beacon=max(nb, 1), n_recent=nr, mode=mode,
                                device=dev, timing=True)
         Kp = torch.randn(LB, Hkv, B_min, D, generator=g, device=dev, dtype=torch.bfloat16)
@@ -350,6 +354,37 @@ def trace_measure(w, dev, B_max=4096, pool=16):
                      "library_us_per_step": round(dev_us / n, 2)}
         del drv, kk, vv, qq
         torch.cuda.empty_cache()
+    return res
+
+
+def diagnostics_measure(w, dev, B=4, B_max=1024, cycles=8):
+    """Synthetic quality diagnostics (paper_2609_04971_amd.diagnostics) on
+    the Qwen3-4B head shape: a revisit trace (32 thought keys per kv-head
+    in 4 groups; 2 % global queries, each aimed at one group; the rest
+    local queries drifting slowly with the recent keys) runs through
+    the periodic driver under Continual FPS beacons (16 + 16), running-mean
+    beacons (16 + 16) and recent queries only (32); per policy the planted
+    keys still cached after each eviction and the max-cosine coverage of
+    the next 256 steps' queries by the observation set (Figure 6a's
+    quantity), over all of them and over the global ones."""
+    import torch
+
+    from paper_2609_04971_amd import diagnostics, synth
+
+    T = B_max + cycles * (B_max // 8)
+    gen = {"n_plant": 32, "n_groups": 4, "p_global": 0.02, "local_dim": 16, "drift": 0.18, "align": 0.8,
+           "local_gain": 0.5, "global_gain": 2.0, "sigma": 0.3}
+    tr = synth.revisit_trace(B, w.Hq, w.Hkv, w.D, T, seed=11, device=dev, **gen)
+    res = {"config": dict(gen, B=B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, B_max=B_max, steps=T, prompt=B_max // 2,
+                          horizon=256)}
+    t0 = time.perf_counter()
+    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("rpc", 16, 32)):
+        r = diagnostics.run(tr, mode, B_max, n_beacon=nb, n_recent=nr, horizon=256)
+        res[mode] = dict(diagnostics.summary(r), n_beacon=0 if mode == "rpc" else nb, n_recent=nr)
+        print(f"# diagnostics {mode}: {res[mode]}", file=sys.stderr, flush=True)
+    res["wall_s"] = round(time.perf_counter() - t0, 1)
+    del tr
+    torch.cuda.empty_cache()
     return res
 
 

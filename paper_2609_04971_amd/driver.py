@@ -25,6 +25,9 @@ this module keeps the per-head state of Algorithm 2 and makes the calls:
 
 mode "rpc" is the recent-queries-only baseline on the same kernels: no
 buffer, no beacons (C = 0), the last n_recent queries before each eviction.
+mode "ns" keeps running-mean beacons instead of the FPS buffer: every
+step's pre-RoPE queries join the nearest of G * n_beacon slots per kv-head
+(bkv_beacon_update), and evictions score with those beacons as they stand.
 
 Everything that computes runs in the library's kernels; this module only
 slices the caller's tensors and appends rows to them (the writes a serving
@@ -46,15 +49,15 @@ class PeriodicEviction:
         rotated to the step at which eviction runs).  record keeps every
         call's inputs and outputs in `events`; timing brackets every library
         call with HIP events on the current stream, in `times`."""
-        if mode not in ("beacon", "rpc"):
-            raise ValueError("mode is 'beacon' or 'rpc'")
+        if mode not in ("beacon", "rpc", "ns"):
+            raise ValueError("mode is 'beacon', 'rpc' or 'ns'")
         if B_max % 8:
             raise ValueError("B_max must be a multiple of 8 (B_min = 7/8 B_max)")
         self.mode = mode
         self.LB, self.Hq, self.Hkv, self.D = layers * B, Hq, Hkv, D
         self.G = Hq // Hkv
         self.B_max, self.B_min = B_max, 7 * B_max // 8
-        self.nb = n_beacon if mode == "beacon" else 0
+        self.nb = 0 if mode == "rpc" else n_beacon
         self.nr = n_recent
         if self.B_max - self.nr <= self.B_min:
             raise ValueError("the recent window must fit between B_min and B_max")
@@ -115,6 +118,14 @@ class PeriodicEviction:
         self.K[:, :, :T] = K
         self.V[:, :, :T] = V
         self.L = self.t = T
+        if self.mode == "ns":
+            # bkv_beacon_update takes queries t-major, so consecutive prompt
+            # chunks give the same running means as one call; chunks keep
+            # each call's element count within the library's 32-bit limit
+            tc = max(1, (2 ** 31 - 1) // (self.LB * self.Hq * self.D))
+            for t0 in range(0, T, tc):
+                qc = q_pre[:, :, t0:t0 + tc].contiguous()
+                self._call("beacon_update", lambda: bkv.beacon_update(self.dims, qc, self.beacons, self.counts))
         if self.mode == "beacon":
             picks = torch.empty(self.LB, self.Hq, min(self.nb, T), dtype=torch.int32, device=K.device)
             self._call("fps_prefill", lambda: bkv.fps_gather(q_pre, self.nb, dst=self.obs, picks=picks))
@@ -129,6 +140,9 @@ class PeriodicEviction:
         self.L += 1
         self.t += 1
         L, nb, nr = self.L, self.nb, self.nr
+        if self.mode == "ns":
+            q_new = q_pre.reshape(self.LB, self.Hq, 1, self.D).contiguous()
+            self._call("beacon_update", lambda: bkv.beacon_update(self.dims, q_new, self.beacons, self.counts))
         if self.mode == "beacon":
             if L <= self.B_max - nr:
                 self.obs[:, :, self.obs_len] = q_pre

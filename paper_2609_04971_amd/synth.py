@@ -185,3 +185,67 @@ def sorted_subsets(P: int, N: int, n: int, seed: int = 0, forced_tail: int = 0):
         tail = torch.arange(N - forced_tail, N)
         out[p] = torch.cat([body, tail]).sort().values.to(torch.int32)
     return out
+
+
+def revisit_trace(LB: int, Hq: int, Hkv: int, D: int, T: int, n_plant: int = 32, n_groups: int = 4,
+                  p_global: float = 0.02, local_dim: int = 16, drift: float = 0.18, align: float = 0.8,
+                  local_gain: float = 0.5, global_gain: float = 2.0, sigma: float = 0.3, seed: int = 0,
+                  device="cpu"):
+    """A decode trace with the query geometry of Section 3 (no RoPE, so
+    queries are their own pre- and post-RoPE forms):
+      * local queries: each kv-head has a direction d(t) that drifts slowly
+        on the unit sphere of a random local_dim-dimensional subspace
+        (d(t) = normalise(d(t-1) + drift * xi), xi ~ N(0, I/local_dim)); key
+        j is sqrt(D) * (align * d(j) + sqrt(1 - align^2) * z_j), z_j a random
+        unit vector, and a local query is local_gain * sqrt(D) * (d(t) +
+        sigma * xi') with xi' ~ N(0, I/D).  Local queries are close to their
+        neighbours and attend to recent keys (Section 3.1, the local
+        pattern; Figure 5a's neighbour similarity);
+      * thought keys: the first n_plant tokens are sqrt(D) * p_i, p_i random
+        unit vectors, in n_groups contiguous groups (the plan and
+        constraints written early in a trace);
+      * global queries: with probability p_global per query head and step
+        (never in the first n_plant steps), a query of a random group c is
+        global_gain * sqrt(D) * (u_c + sigma * xi'), u_c the normalised sum
+        of the group's p_i.  Global queries of one group are close to each
+        other and far from their local neighbours, and attend to their
+        group's thought keys (Section 3.1, thought revisiting; Section 3.2,
+        the clusters of Figure 5b).
+    Returns K, V [LB, Hkv, T, D] bf16, q [LB, Hq, T, D] bf16, is_global
+    [LB, Hq, T] bool, group [LB, Hq, T] int64 (-1 for local queries) and
+    n_plant."""
+    g = _gen(seed, device)
+    G = Hq // Hkv
+    sq = math.sqrt(D)
+    basis = torch.linalg.qr(torch.randn(LB, Hkv, D, local_dim, generator=g, device=device))[0]
+    x = torch.randn(LB, Hkv, local_dim, generator=g, device=device)
+    walk = torch.empty(LB, Hkv, T, local_dim, device=device)
+    steps = torch.randn(LB, Hkv, T, local_dim, generator=g, device=device) * (drift / math.sqrt(local_dim))
+    x = x / x.norm(dim=-1, keepdim=True)
+    for t in range(T):
+        x = x + steps[:, :, t]
+        x = x / x.norm(dim=-1, keepdim=True)
+        walk[:, :, t] = x
+    d = torch.matmul(walk, basis.transpose(-1, -2))  # [LB, Hkv, T, D] unit
+    z = torch.randn(LB, Hkv, T, D, generator=g, device=device)
+    z = z / z.norm(dim=-1, keepdim=True)
+    K = sq * (align * d + math.sqrt(1.0 - align * align) * z)
+    p = torch.randn(LB, Hkv, n_plant, D, generator=g, device=device)
+    p = p / p.norm(dim=-1, keepdim=True)
+    K[:, :, :n_plant] = sq * p
+    V = torch.randn(LB, Hkv, T, D, generator=g, device=device)
+    grp_of = torch.arange(n_plant, device=device) * n_groups // n_plant
+    u = torch.zeros(LB, Hkv, n_groups, D, device=device).index_add_(2, grp_of, p)
+    u = u / u.norm(dim=-1, keepdim=True)
+    is_global = torch.rand(LB, Hq, T, generator=g, device=device) < p_global
+    is_global[:, :, :n_plant] = False
+    group = torch.randint(0, n_groups, (LB, Hq, T), generator=g, device=device)
+    kv = (torch.arange(Hq, device=device) // G).view(1, Hq, 1).expand(LB, Hq, T)
+    b = torch.arange(LB, device=device).view(LB, 1, 1).expand(LB, Hq, T)
+    xi = torch.randn(LB, Hq, T, D, generator=g, device=device) / sq
+    q_loc = local_gain * sq * (d.repeat_interleave(G, dim=1) + sigma * xi)
+    q_glb = global_gain * sq * (u[b, kv, group] + sigma * xi)
+    q = torch.where(is_global.unsqueeze(-1), q_glb, q_loc)
+    group = torch.where(is_global, group, torch.full_like(group, -1))
+    return {"K": K.to(torch.bfloat16), "V": V.to(torch.bfloat16), "q": q.to(torch.bfloat16).contiguous(),
+            "is_global": is_global, "group": group, "n_plant": n_plant}
