@@ -7,15 +7,20 @@
 // of largest cosine similarity (ties -> lowest slot, cosine 0 when a norm is
 // 0) and that slot moves to the running mean of its members.
 //
-// One wave per (batch, kv-head); the T*G queries of the head's group are
-// processed strictly in order (t-major, then g), each seeing the previous
-// update.  The head's beacons live in LDS (rows padded to D + 4 floats so
-// that sixteen lanes reading 16-byte vectors of sixteen different slots hit
-// distinct banks) together with their squared norms, which are kept up to
-// date as slots change.  Per query, lane c accumulates slot c's dot product
-// over D with 16-byte LDS reads; all lanes share the query's squared norm;
-// an argmax over lanes picks the slot, and the lanes update that slot's D
-// coordinates and its norm in parallel.  The step is latency-bound.
+// One workgroup of 256 threads per (batch, kv-head).  The head's beacons live
+// in LDS (rows padded to D + 4 floats so that sixteen lanes reading 16-byte
+// vectors of sixteen different slots hit distinct banks) together with their
+// squared norms, which are kept up to date as slots change.  All four waves
+// bring the beacons in (every 16-byte load of the head issued before any is
+// waited on: one HBM round trip) and compute the norms (four threads per
+// slot).  Then one wave takes the T*G queries of the head's group strictly
+// in order (t-major, then g), each seeing the previous update: lane c
+// accumulates slot c's dot product over D with 16-byte LDS reads; an argmax
+// over lanes (DPP, no LDS round trip) picks the slot; the lanes update that
+// slot's D coordinates and its norm in parallel.  Finally the four waves
+// write back the slots that changed (at most T*G of the C rows; the others
+// still hold what was read).  The LDS is sized by C, so small C leaves room
+// for more heads per CU.
 #include <math.h>
 
 #include "device_common.h"
@@ -24,19 +29,15 @@
 namespace bkv {
 namespace {
 
-constexpr int kMaxC = 64;
-
-template <typename T>
-__device__ __forceinline__ float load_elem(const T* p, size_t i);
-template <>
-__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, size_t i) { return dev::bf16_to_f32(p[i]); }
-template <>
-__device__ __forceinline__ float load_elem<float>(const float* p, size_t i) { return p[i]; }
+// Query elements are loaded raw and widened only where they are used, so
+// that a prefetch is not waited on right after it is issued.
+__device__ __forceinline__ float widen(uint16_t v) { return dev::bf16_to_f32(v); }
+__device__ __forceinline__ float widen(float v) { return v; }
 
 // Dot product of two D-float rows in LDS (16-byte aligned), with four
 // independent partial sums so that the FMAs do not wait on each other.
 template <int D>
-__device__ __forceinline__ float row_dot_impl(const float* a, const float* b) {
+__device__ __forceinline__ float row_dot(const float* a, const float* b) {
     const float4* ar = reinterpret_cast<const float4*>(a);
     const float4* br = reinterpret_cast<const float4*>(b);
     float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
@@ -51,63 +52,107 @@ __device__ __forceinline__ float row_dot_impl(const float* a, const float* b) {
     return (p0 + p1) + (p2 + p3);
 }
 
-// Sum over the wave (all 64 lanes hold the result).
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += dev::shfl_xor_f(v, o);
-    return v;
+// Orders the calling wave's LDS accesses for the compiler: one lane's
+// write before the fence is seen by another lane's read after it.  A wave's
+// LDS instructions execute in order, so a wavefront-scope fence needs no
+// wait instruction; in particular it does not wait for the next query's
+// global loads in flight (a workgroup-scope fence or barrier would).  The
+// query loop runs on one wave while the others wait at a later barrier, so
+// it could not use the workgroup barrier anyway.
+__device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
+
+constexpr int kThreads = 256;
+constexpr int kMaxSlots = 64;  // the boundary rejects C > 64: one bit per slot in a 64-bit mask
+
+// LDS bytes of one head: C padded beacon rows, the current query, C norms,
+// C counts, the mask of changed slots.
+template <int D>
+constexpr size_t smem_bytes(int C) {
+    return ((size_t)C * (D + 4) + D + C) * sizeof(float) + (size_t)C * sizeof(int) + sizeof(unsigned long long);
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(64) void beacon_update_kernel(const T* __restrict__ q_new, int T_steps, float* beacons,
-                                                           int32_t* counts, int32_t* assign, int Hq, int Hkv, int C) {
-    constexpr int LD = D + 4;        // padded row: 16-byte reads of 16 slots hit distinct banks
-    constexpr int PER = D / 64;      // coordinates per lane in lane-parallel loops
-    __shared__ __attribute__((aligned(16))) float bl[kMaxC * LD];
-    __shared__ __attribute__((aligned(16))) float xs[D];
-    __shared__ float bn2[kMaxC];     // squared norm of each slot
-    __shared__ int cnt[kMaxC];
-    auto row_dot = [](const float* a, const float* b) { return row_dot_impl<D>(a, b); };
-    const int lane = threadIdx.x;
+__global__ __launch_bounds__(kThreads) void beacon_update_kernel(const T* __restrict__ q_new, int T_steps,
+                                                                 float* beacons, int32_t* counts, int32_t* assign,
+                                                                 int Hq, int Hkv, int C) {
+    constexpr int LD = D + 4;                         // padded row
+    constexpr int PER = D / 64;                       // coordinates per lane in lane-parallel loops
+    constexpr int kLoads = kMaxSlots * D / 4 / kThreads;  // 16-byte beacon loads per thread at most
+    extern __shared__ __attribute__((aligned(16))) float smem[];
+    float* bl = smem;                                 // [C][LD]
+    float* xs = bl + C * LD;                          // [D], 16-byte aligned: C * LD and D are multiples of 4
+    float* bn2 = xs + D;                              // [C] squared norm of each slot
+    int* cnt = reinterpret_cast<int*>(bn2 + C);       // [C]
+    unsigned long long* dirty_out = reinterpret_cast<unsigned long long*>(cnt + C);  // 8-byte aligned
+    const int tid = threadIdx.x, lane = tid & 63;
+    const bool seq_wave = tid < 64;
     const int h = blockIdx.x, b = h / Hkv, kh = h % Hkv;
     const int G = Hq / Hkv;
     float* bh = beacons + (size_t)h * C * D;
-    // query q = t * G + g; its coordinates are loaded one query ahead (the
-    // first one before the beacons)
     const int nq = T_steps * G;
     auto query_ptr = [&](int qq) {
         const int t = qq / G, g = qq - t * G;
         return q_new + (((size_t)b * Hq + (size_t)kh * G + g) * T_steps + t) * D;
     };
-    float xnext[PER];
+    // The first query, the counts and every beacon vector of the head are
+    // loaded unconditionally (threads past the end re-read the last element)
+    // and pinned by an empty asm before the first store uses them, so the
+    // compiler can neither sink a load into the guarded store nor wait
+    // between loads: all of them issue before the first wait.
+    T xnext[PER];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) xnext[k] = load_elem<T>(query_ptr(0), lane + 64 * k);
-    // beacons in with 16-byte loads (D is a multiple of 4 and rows are 16-byte aligned)
-    for (int i = lane; i < C * D / 4; i += 64) {
-        const float4 v = reinterpret_cast<const float4*>(bh)[i];
-        const int c = (4 * i) / D, d = (4 * i) % D;
-        *reinterpret_cast<float4*>(&bl[c * LD + d]) = v;
+    for (int k = 0; k < PER; ++k) xnext[k] = query_ptr(0)[lane + 64 * k];
+    const int n4 = C * D / 4;
+    dev::u32x4 v[kLoads];
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) v[k] = reinterpret_cast<const dev::u32x4*>(bh)[min(tid + kThreads * k, n4 - 1)];
+    int cv = counts[(size_t)h * C + min(tid, C - 1)];
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) asm volatile("" : "+v"(v[k]));
+    asm volatile("" : "+v"(cv));
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) {
+        const int i = tid + kThreads * k;
+        if (i < n4) *reinterpret_cast<dev::u32x4*>(&bl[(4 * i) / D * LD + (4 * i) % D]) = v[k];
     }
-    if (lane < C) cnt[lane] = counts[(size_t)h * C + lane];
+    if (tid < C) cnt[tid] = cv;
     __syncthreads();
-    if (lane < C) bn2[lane] = row_dot(&bl[lane * LD], &bl[lane * LD]);  // squared norms
+    // squared norms: four threads (one quad) per slot, D/4 coordinates each
+    {
+        const int c = tid >> 2, part = tid & 3;
+        float p = 0.f;
+        if (c < C) {
+            const float4* r = reinterpret_cast<const float4*>(&bl[c * LD + part * (D / 4)]);
+#pragma unroll
+            for (int d4 = 0; d4 < D / 16; ++d4) {
+                const float4 u = r[d4];
+                p = fmaf(u.x, u.x, p);
+                p = fmaf(u.y, u.y, p);
+                p = fmaf(u.z, u.z, p);
+                p = fmaf(u.w, u.w, p);
+            }
+        }
+        p = dev::quad_sum(p);
+        if (c < C && part == 0) bn2[c] = p;
+    }
     __syncthreads();
 
-    for (int q = 0; q < nq; ++q) {
-        {
+    if (seq_wave) {
+        unsigned long long dirty = 0;  // slots changed (wave-uniform)
+        for (int q = 0; q < nq; ++q) {
             float xn = 0.f;
 #pragma unroll
             for (int k = 0; k < PER; ++k) {
-                const float v = xnext[k];
-                xs[lane + 64 * k] = v;
-                xn = fmaf(v, v, xn);
+                const float x = widen(xnext[k]);
+                xs[lane + 64 * k] = x;
+                xn = fmaf(x, x, xn);
             }
-            if (q + 1 < nq) {
+            // the next query (the last one again at the end: no branch to
+            // join, so nothing waits for it before its use)
 #pragma unroll
-                for (int k = 0; k < PER; ++k) xnext[k] = load_elem<T>(query_ptr(q + 1), lane + 64 * k);
-            }
-            xn = wave_sum(xn);
-            __syncthreads();
+            for (int k = 0; k < PER; ++k) xnext[k] = query_ptr(min(q + 1, nq - 1))[lane + 64 * k];
+            xn = dev::wave_sum(xn);
+            wave_lds_fence();
             // lowest empty slot, if any
             const unsigned long long empty = __ballot(lane < C && cnt[lane] == 0);
             int chosen;
@@ -120,22 +165,14 @@ __global__ __launch_bounds__(64) void beacon_update_kernel(const T* __restrict__
                     bn2[chosen] = xn;
                 }
             } else {
-                const float dot = (lane < C) ? row_dot(&bl[lane * LD], xs) : 0.f;
+                const float dot = (lane < C) ? row_dot<D>(&bl[lane * LD], xs) : 0.f;
                 const float bn = (lane < C) ? bn2[lane] : 0.f;
-                float cs = (xn == 0.f || bn == 0.f) ? 0.f : dot / (sqrtf(xn) * sqrtf(bn));
-                if (lane >= C) cs = -INFINITY;
-                int idx = lane;
-                // argmax over lanes, ties -> lowest slot
-#pragma unroll
-                for (int o = 32; o > 0; o >>= 1) {
-                    const float oc = dev::shfl_xor_f(cs, o);
-                    const int oi = dev::shfl_xor_i(idx, o);
-                    if (oc > cs || (oc == cs && oi < idx)) {
-                        cs = oc;
-                        idx = oi;
-                    }
-                }
-                chosen = idx;
+                const float cs = (xn == 0.f || bn == 0.f) ? 0.f : dot / (sqrtf(xn) * sqrtf(bn));
+                // argmax over the slots, ties -> lowest slot: the minimum of
+                // (inverted order key of the cosine, slot)
+                const unsigned long long key =
+                    lane < C ? ((unsigned long long)(~dev::ord_key(cs)) << 32) | (unsigned)lane : ~0ull;
+                chosen = (int)(unsigned)dev::wave_min_u64(key);
                 const int n = cnt[chosen] + 1;
                 const float inv = 1.0f / (float)n;
                 float p = 0.f;
@@ -147,21 +184,26 @@ __global__ __launch_bounds__(64) void beacon_update_kernel(const T* __restrict__
                     bl[chosen * LD + d] = nv;
                     p = fmaf(nv, nv, p);
                 }
-                p = wave_sum(p);
+                p = dev::wave_sum(p);
                 if (lane == 0) {
                     cnt[chosen] = n;
                     bn2[chosen] = p;
                 }
             }
+            dirty |= 1ull << chosen;
             if (assign && lane == 0) assign[(size_t)h * T_steps * G + q] = chosen;
-            __syncthreads();
+            wave_lds_fence();
         }
+        if (lane == 0) *dirty_out = dirty;
     }
-    for (int i = lane; i < C * D / 4; i += 64) {
+    __syncthreads();
+    // write back the changed slots only: the others still hold what was read
+    const unsigned long long dirty = *dirty_out;
+    for (int i = tid; i < n4; i += kThreads) {
         const int c = (4 * i) / D, d = (4 * i) % D;
-        reinterpret_cast<float4*>(bh)[i] = *reinterpret_cast<const float4*>(&bl[c * LD + d]);
+        if ((dirty >> c) & 1ull) reinterpret_cast<float4*>(bh)[i] = *reinterpret_cast<const float4*>(&bl[c * LD + d]);
     }
-    if (lane < C) counts[(size_t)h * C + lane] = cnt[lane];
+    if (tid < C && ((dirty >> tid) & 1ull)) counts[(size_t)h * C + tid] = cnt[tid];
 }
 
 }  // namespace
@@ -172,8 +214,8 @@ hipError_t launch_beacon_update(const bkv_dims& d, const void* q_new, int T, flo
     if (P == 0 || T == 0) return hipSuccess;
     const bool bf = d.dtype == BKV_BF16;
 #define BKV_LAUNCH_BU(TY, DD)                                                                                   \
-    hipLaunchKernelGGL((beacon_update_kernel<TY, DD>), dim3(P), dim3(64), 0, s, static_cast<const TY*>(q_new), T, \
-                       beacons, counts, assign, d.Hq, d.Hkv, d.C)
+    hipLaunchKernelGGL((beacon_update_kernel<TY, DD>), dim3(P), dim3(kThreads), smem_bytes<DD>(d.C), s,                   \
+                       static_cast<const TY*>(q_new), T, beacons, counts, assign, d.Hq, d.Hkv, d.C)
     if (bf && d.D == 128)
         BKV_LAUNCH_BU(uint16_t, 128);
     else if (bf)

@@ -1,5 +1,5 @@
 // Device helpers shared by the gfx950 kernels: scoped atomics, a bounded
-// wait, wave shuffles and bf16 rounding.
+// wait, wave shuffles and DPP reductions, and bf16 rounding.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -82,6 +82,59 @@ __device__ inline bool stamp_ok(const int* hdr, int P, int budget) {
 
 __device__ inline float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, 64); }
 __device__ inline int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, 64); }
+
+// Wave reductions over all 64 lanes without an LDS round trip: DPP swaps
+// within quads (quad_perm [1,0,3,2], then [2,3,0,1]), the half-row mirror
+// and the row mirror leave every lane of a 16-lane row holding the row's
+// result; the four row results are then combined as scalars (readlane), so
+// the answer is wave-uniform.  All 64 lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_min_u32(unsigned v) {
+    const unsigned w = (unsigned)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+    return w < v ? w : v;
+}
+
+__device__ __forceinline__ unsigned wave_min_u32(unsigned v) {
+    v = dpp_min_u32<0xb1>(v);
+    v = dpp_min_u32<0x4e>(v);
+    v = dpp_min_u32<0x141>(v);
+    v = dpp_min_u32<0x140>(v);
+    const unsigned a = (unsigned)__builtin_amdgcn_readlane((int)v, 0), b = (unsigned)__builtin_amdgcn_readlane((int)v, 16);
+    const unsigned c = (unsigned)__builtin_amdgcn_readlane((int)v, 32), d = (unsigned)__builtin_amdgcn_readlane((int)v, 48);
+    return min(min(a, b), min(c, d));
+}
+
+// Lexicographic minimum of 64-bit keys over the wave: the high words first,
+// then the low words of the lanes that hold it.
+__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
+    const unsigned hi = wave_min_u32((unsigned)(v >> 32));
+    const unsigned lo = wave_min_u32((unsigned)(v >> 32) == hi ? (unsigned)v : 0xffffffffu);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+// Order-preserving map of a float to an unsigned key (-0 counts as +0).
+__device__ __forceinline__ unsigned ord_key(float f) {
+    unsigned u = __float_as_uint(f == 0.f ? 0.f : f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float v) {
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+// Sum within each quad of lanes (all four lanes hold it).
+__device__ __forceinline__ float quad_sum(float v) { return dpp_add<0x4e>(dpp_add<0xb1>(v)); }
+
+// Sum over the wave, the same in every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+    v = dpp_add<0x140>(dpp_add<0x141>(quad_sum(v)));
+    const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (a + b) + (c + d);
+}
 
 // bf16 <-> fp32.  bf16 is the top half of binary32; rounding is to
 // nearest, ties to even, and NaN stays NaN.

@@ -246,35 +246,6 @@ __global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows
 
 // ---- n up to 32768: rows streamed per pick, 1024 threads per head -----------------
 
-template <int CTRL>
-__device__ __forceinline__ unsigned dpp_min_u32(unsigned v) {
-    const unsigned w = (unsigned)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
-    return w < v ? w : v;
-}
-
-__device__ __forceinline__ unsigned wave_min_u32(unsigned v) {
-    v = dpp_min_u32<0xb1>(v);
-    v = dpp_min_u32<0x4e>(v);
-    v = dpp_min_u32<0x141>(v);
-    v = dpp_min_u32<0x140>(v);
-    const unsigned a = (unsigned)__builtin_amdgcn_readlane((int)v, 0), b = (unsigned)__builtin_amdgcn_readlane((int)v, 16);
-    const unsigned c = (unsigned)__builtin_amdgcn_readlane((int)v, 32), d = (unsigned)__builtin_amdgcn_readlane((int)v, 48);
-    return min(min(a, b), min(c, d));
-}
-
-// Lexicographic minimum of 64-bit keys over the wave (all lanes active):
-// the high words first, then the low words of the lanes that hold it.
-__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
-    const unsigned hi = wave_min_u32((unsigned)(v >> 32));
-    const unsigned lo = wave_min_u32((unsigned)(v >> 32) == hi ? (unsigned)v : 0xffffffffu);
-    return ((unsigned long long)hi << 32) | lo;
-}
-// Order-preserving map of a float to an unsigned key (-0 counts as +0).
-__device__ __forceinline__ unsigned ord_key(float f) {
-    unsigned u = __float_as_uint(f == 0.f ? 0.f : f);
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
 // Row loads are issued eight 16-byte chunks at a time, so that at most 32
 // registers hold loads in flight next to the per-row state.
 constexpr int kChunkGroup = 8;
@@ -394,14 +365,14 @@ __global__ __launch_bounds__(kStreamThreads) void fps_stream_kernel(const T* src
         float binv = 0.f;
         dev::static_for<RPT>([&](auto i) {
             if (!((done >> i) & 1ull)) {
-                const unsigned long long key = ((unsigned long long)ord_key(S[i]) << 32) | (unsigned)(t + NT * i);
+                const unsigned long long key = ((unsigned long long)dev::ord_key(S[i]) << 32) | (unsigned)(t + NT * i);
                 if (key < best) {
                     best = key;
                     binv = inv[i];
                 }
             }
         });
-        const unsigned long long wbest = wave_min_u64(best);
+        const unsigned long long wbest = dev::wave_min_u64(best);
         if (wbest == ~0ull) {
             if (lane == 0) wkey[wave] = wbest;
         } else if (best == wbest) {  // keys are unique: exactly one lane
