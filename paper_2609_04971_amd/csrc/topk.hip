@@ -7,21 +7,30 @@
 // N <= budget every token is kept.
 //
 // One 1024-thread workgroup per head.  Scores map to a monotone uint32 key
-// (-0 first canonicalised to +0), and an exact radix select with 8-bit
-// digits (4 passes, LDS histograms per wave) finds the k_sel-th largest
+// (-0 first canonicalised to +0); the selection finds the k_sel-th largest
 // candidate key theta and how many candidates equal to theta are taken.
-// The emit pass needs no sort: each thread owns a contiguous run of indices,
-// and two block-wide exclusive scans (ties taken so far, kept so far) give
-// every kept index its output position in ascending order.
+// The emit needs no sort: block-wide exclusive scans (ties taken so far,
+// kept so far) give every kept index its output position in ascending
+// order.
 //
 // Up to 32768 tokens the head's keys are read from HBM once, coalesced, and
-// held in registers (32 per thread, token tid + 1024 i) through the radix
-// passes.  Digit counts use four histogram copies per wave, and the wave's
-// most common digit is added once by one lane, since same-address LDS
-// atomics serialise.  The emit pass ranks kept tokens with ballots: a
-// wave's 64 consecutive tokens are ranked by mbcnt, and one block scan over
-// the per-wave counts in token order gives each run its base.  Longer heads
-// stream the scores from memory on every pass and emit from contiguous
+// held in registers (32 per thread, token tid + 1024 i).  A first stage
+// bins the candidates by value, linearly over [min, max] of their scores
+// into 4096 bins (the map is monotone under rounding, so a higher bin beats
+// a lower one).  Bits of the float key would follow its exponent and put a
+// whole head in a handful of bins; value bins spread a head's keys over
+// many, and the bin holding the threshold usually has a few dozen.  Up to
+// 512 of them are ranked directly by (key descending, token ascending),
+// which gives theta and the ties to take; more (many equal or nearly equal
+// scores), or NaN / +inf candidates, go through an exact radix select with
+// 8-bit digits over the bits that vary, whose counts use four histogram
+// copies per wave and add the wave's most common digit once, by one lane,
+// since same-address LDS atomics serialise.  Ties at theta are
+// ranked in token order only when some of them must be left out.  The emit
+// ranks kept tokens with ballots: a wave's 64 consecutive tokens are ranked
+// by mbcnt, and one block scan over the per-wave counts in token order
+// gives each run its base.  Longer heads stream the scores from memory on
+// every pass (8-bit radix digits from the top) and emit from contiguous
 // per-thread runs.
 #include "device_common.h"
 #include "internal.h"
@@ -217,6 +226,26 @@ constexpr int kPer = kRegKeys / kThreads;  // keys per thread
 constexpr int kSub = 4;                      // histogram copies per wave
 constexpr int kRows = kPer * kWaves;         // (row i, wave) runs of 64 tokens
 
+// Block-wide suffix scan of the kBins first-stage counts (thread t owns the
+// bins of its reversed index rt = kThreads - 1 - t, 4 rt .. 4 rt + 3, so the
+// exclusive prefix in thread order counts every higher bin): the bin at
+// which the running count from the top reaches `remaining`, and how many
+// candidates lie strictly above it.
+__device__ __forceinline__ void find_wide_digit(const int* cnt, int remaining, int* buf, int* s_digit,
+                                                int* s_above) {
+    const int rt = kThreads - 1 - (int)threadIdx.x;
+    const int d0 = 4 * rt;
+    const int c0 = cnt[d0], c1 = cnt[d0 + 1], c2 = cnt[d0 + 2], c3 = cnt[d0 + 3];
+    int total;
+    const int above = block_excl_scan(c0 + c1 + c2 + c3, buf, &total);  // bins >= 4 (rt + 1)
+    const int S3 = above + c3, S2 = S3 + c2, S1 = S2 + c1, S0 = S1 + c0;
+    const int r = remaining;
+    if (S3 >= r && above < r) { *s_digit = d0 + 3; *s_above = above; }
+    if (S2 >= r && S3 < r) { *s_digit = d0 + 2; *s_above = S3; }
+    if (S1 >= r && S2 < r) { *s_digit = d0 + 1; *s_above = S2; }
+    if (S0 >= r && S1 < r) { *s_digit = d0; *s_above = S1; }
+}
+
 // Add one to digit d of this lane's histogram copy.  The most common digit
 // among the wave's active lanes is counted with one atomic by its first lane
 // (digits are often concentrated, and same-address LDS atomics serialise);
@@ -248,20 +277,61 @@ __device__ __forceinline__ void scan_runs(int* c, int* buf) {
     __syncthreads();
 }
 
+// Float min / max over the block through order keys (DPP within waves, LDS
+// across them); `slot` holds kWaves words.  Every thread gets the result.
+__device__ __forceinline__ uint32_t block_min_u32(uint32_t v, uint32_t* slot) {
+    v = dev::wave_min_u32(v);
+    if ((threadIdx.x & 63) == 0) slot[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint32_t m = slot[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) m = min(m, slot[w]);
+    __syncthreads();
+    return m;
+}
+__device__ __forceinline__ float key_to_float(uint32_t k) {  // inverse of order_key (on keys it produces)
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// OR over the wave (DPP within rows, then the four rows), wave-uniform.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_or(uint32_t v) {
+    return v | (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint32_t wave_or_u32(uint32_t v) {
+    v = dpp_or<0x140>(dpp_or<0x141>(dpp_or<0x4e>(dpp_or<0xb1>(v))));
+    return (uint32_t)(__builtin_amdgcn_readlane((int)v, 0) | __builtin_amdgcn_readlane((int)v, 16) |
+                      __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
+}
+
+constexpr int kBins = 4096;    // value bins of the first stage
+constexpr int kMaxRank = 512;  // candidates ranked directly at most
+
+// Value bin of score v: monotone non-decreasing in v (each step is a
+// correctly rounded operation or a clamp), so every key in a higher bin
+// beats every key in a lower one.  -inf lands in bin 0.
+__device__ __forceinline__ int value_bin(float v, float vmin, float scale) {
+    const float t = (v - vmin) * scale;
+    return (int)fminf(fmaxf(floorf(t), 0.f), (float)(kBins - 1));
+}
+
 __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restrict__ scores,
                                                              int32_t* __restrict__ kept, int N, int budget, int W,
                                                              int n_prefix, int n_keep) {
+    // per-wave 8-bit histograms; the value histogram and the candidate list
+    // of the first stage reuse the same memory before them
     __shared__ int hist[kWaves][kSub][256];
+    static_assert(kWaves * kSub * 256 >= kBins + 2 * kMaxRank, "LDS reuse");
     __shared__ int part[kThreads / 256][256];
     __shared__ int tot[256];
     __shared__ int runs[kRows];
     __shared__ int scan_buf[kWaves + 1];
-    __shared__ uint32_t red_min[kWaves], red_max[kWaves];
-    __shared__ int s_digit, s_above;
+    __shared__ uint32_t red[kWaves];
+    __shared__ uint32_t red3[3][kWaves];
+    __shared__ int s_digit, s_above, s_ncand, s_need, s_eqtot;
+    __shared__ uint32_t s_theta;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int sub = lane >> 4;
-    uint32_t key_lo = 0;
-    int vbits = 0;
     const int h = blockIdx.x;
     const float* srow = scores + (size_t)h * N;
     int32_t* out = kept + (size_t)h * n_keep;
@@ -276,48 +346,145 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
     uint32_t u[kPer];
 #pragma unroll
     for (int i = 0; i < kPer; ++i) u[i] = order_key(srow[min(tid + i * kThreads, N - 1)]);
-    uint32_t cand = 0;
+    uint32_t pos_cand = 0;  // candidate positions (the rest are forced keeps or past N)
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
         const int j = tid + i * kThreads;
-        if (j >= lo && j < hi) cand |= 1u << i;
+        if (j >= lo && j < hi) pos_cand |= 1u << i;
     }
-    // Radix select on v = key - (smallest candidate key) over only the bits
-    // that vary: the first digit then spreads over the occupied range
-    // instead of a few exponent values.
-    {
+    uint32_t comp = pos_cand;  // candidates still competing for the remaining places
+    uint32_t sure = 0;         // candidates kept whatever the threshold
+    int remaining = ksel;
+    bool decided = false;      // theta and need_eq known
+    uint32_t theta = 0;
+    int need_eq = 0;
+    int eq_total = -1;         // candidates equal to theta, when known
+    if (tid == 0) {
+        s_ncand = 0;
+        s_need = 0;
+        s_eqtot = 0;
+    }
+    __syncthreads();  // the counters are clear before any wave adds to them
+    if (ksel > 0) {
+        // ---- stage 1: value bins over [vmin, vmax] of the candidates -----------
+        // In key order -inf is kNegInf and the finite scores lie strictly
+        // between it and kPosInf; NaN or +inf candidates take the radix path,
+        // and vmin is the smallest finite score.
+        constexpr uint32_t kNegInf = 0x007fffffu, kPosInf = 0xff800000u;
+        uint32_t kall = 0xffffffffu, kfin = 0xffffffffu, kmx = 0u;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const bool c = (pos_cand >> i) & 1u;
+            kall = min(kall, c ? u[i] : 0xffffffffu);
+            kfin = min(kfin, (c && u[i] > kNegInf) ? u[i] : 0xffffffffu);
+            kmx = max(kmx, c ? u[i] : 0u);
+        }
+        {   // the three minima over the block in one exchange
+            const uint32_t a = dev::wave_min_u32(kall), b = dev::wave_min_u32(kfin), c = dev::wave_min_u32(~kmx);
+            if (lane == 0) {
+                red3[0][wave] = a;
+                red3[1][wave] = b;
+                red3[2][wave] = c;
+            }
+            __syncthreads();
+            kall = red3[0][0];
+            kfin = red3[1][0];
+            uint32_t nmx = red3[2][0];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) {
+                kall = min(kall, red3[0][w]);
+                kfin = min(kfin, red3[1][w]);
+                nmx = min(nmx, red3[2][w]);
+            }
+            kmx = ~nmx;
+        }
+        const bool finite_or_neg_inf = kall >= kNegInf && kmx < kPosInf;
+        const float vmin = key_to_float(kfin), vmax = key_to_float(kmx);
+        const float width = vmax - vmin;
+        const float scale = (float)kBins / width;
+        const bool use_bins = finite_or_neg_inf && kfin < kPosInf && vmax > vmin && width < INFINITY &&
+                              scale < INFINITY;
+        if (use_bins) {
+            int* h1 = &hist[0][0][0];
+            for (int i = tid; i < kBins; i += kThreads) h1[i] = 0;
+            __syncthreads();
+            // value bins are spread, so plain atomics rarely collide
+#pragma unroll
+            for (int i = 0; i < kPer; ++i)
+                if ((pos_cand >> i) & 1u) atomicAdd(&h1[value_bin(key_to_float(u[i]), vmin, scale)], 1);
+            __syncthreads();
+            find_wide_digit(h1, remaining, scan_buf, &s_digit, &s_above);
+            __syncthreads();
+            const int bstar = s_digit;
+            remaining -= s_above;
+            const int ncand = h1[bstar];
+            comp = 0;
+#pragma unroll
+            for (int i = 0; i < kPer; ++i) {
+                const int b = value_bin(key_to_float(u[i]), vmin, scale);
+                sure |= (b > bstar ? 1u : 0u) << i;
+                comp |= (b == bstar ? 1u : 0u) << i;
+            }
+            sure &= pos_cand;
+            comp &= pos_cand;
+            if (ncand <= kMaxRank) {
+                // ---- stage 2a: rank the threshold bin's keys by (key descending,
+                // token ascending); rank remaining - 1 is theta
+                uint32_t* ck = reinterpret_cast<uint32_t*>(h1 + kBins);
+                int* ci = h1 + kBins + kMaxRank;
+                const uint32_t wcomp = wave_or_u32(comp);  // positions where some lane competes
+#pragma unroll
+                for (int i = 0; i < kPer; ++i) {
+                    if (!((wcomp >> i) & 1u)) continue;  // wave-uniform: usually skipped
+                    if ((comp >> i) & 1u) {
+                        const int slot = atomicAdd(&s_ncand, 1);
+                        ck[slot] = u[i];
+                        ci[slot] = tid + i * kThreads;
+                    }
+                }
+                __syncthreads();
+                int rank = kMaxRank;
+                uint32_t mk = 0;
+                if (tid < ncand) {
+                    mk = ck[tid];
+                    const int mi = ci[tid];
+                    rank = 0;
+                    for (int c = 0; c < ncand; ++c) {
+                        const uint32_t k = ck[c];
+                        rank += (k > mk) || (k == mk && ci[c] < mi);
+                    }
+                    if (rank == remaining - 1) s_theta = mk;
+                }
+                __syncthreads();
+                theta = s_theta;
+                if (tid < ncand && mk == theta) {
+                    atomicAdd(&s_eqtot, 1);
+                    if (rank < remaining) atomicAdd(&s_need, 1);
+                }
+                __syncthreads();
+                need_eq = s_need;
+                eq_total = s_eqtot;
+                decided = true;
+            }
+        }
+    }
+    if (ksel > 0 && !decided) {
+        // ---- stage 2b: exact radix select among the competing keys ----------
+        // on v = key - (smallest competing key), over only the bits that vary
         uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
         for (int i = 0; i < kPer; ++i)
-            if ((cand >> i) & 1u) {
+            if ((comp >> i) & 1u) {
                 kmin = min(kmin, u[i]);
                 kmax = max(kmax, u[i]);
             }
+        kmin = block_min_u32(kmin, red);
+        kmax = ~block_min_u32(~kmax, red);
+        const uint32_t key_lo = kmin;
+        const int vbits = (kmax > kmin) ? 32 - __builtin_clz(kmax - kmin) : 0;
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
-            kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
-        }
-        if (lane == 0) {
-            red_min[wave] = kmin;
-            red_max[wave] = kmax;
-        }
-        __syncthreads();
-        kmin = red_min[0];
-        kmax = red_max[0];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) {
-            kmin = min(kmin, red_min[w]);
-            kmax = max(kmax, red_max[w]);
-        }
-        key_lo = kmin;
-        vbits = (kmax > kmin) ? 32 - __builtin_clz(kmax - kmin) : 0;
-    }
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) u[i] -= key_lo;  // candidates only are compared from here on
-    uint32_t prefix = 0, pmask = 0;
-    int remaining = ksel;
-    if (ksel > 0) {
+        for (int i = 0; i < kPer; ++i) u[i] -= key_lo;  // compared only where competing from here on
+        uint32_t prefix = 0, pmask = 0;
         const int npass = (vbits + 7) / 8;
         for (int pass = 0; pass < npass; ++pass) {
             const int shift = max(0, vbits - 8 * (pass + 1));
@@ -327,7 +494,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
             int* hw = &hist[wave][sub][0];
 #pragma unroll
             for (int i = 0; i < kPer; ++i)
-                count_digit(hw, (u[i] >> shift) & 255u, ((cand >> i) & 1u) && (u[i] & pmask) == prefix);
+                count_digit(hw, (u[i] >> shift) & 255u, ((comp >> i) & 1u) && (u[i] & pmask) == prefix);
             __syncthreads();
             {   // digit d's count: thread (d, q) sums the copies of waves 4q..4q+3
                 const int d = tid & 255, q = tid >> 8;
@@ -346,39 +513,43 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
             prefix |= (uint32_t)s_digit << shift;
             pmask |= 255u << shift;
             remaining -= s_above;
+            if (pass == npass - 1) eq_total = tot[s_digit];  // every bit decided: the keys equal to theta
             __syncthreads();
         }
+        theta = prefix;
+        need_eq = remaining;
     }
-    const uint32_t theta = prefix;
-    const int need_eq = (ksel > 0) ? remaining : 0;  // ties at theta to take, lowest index first
-    // Ties: rank of each tied candidate among the tied ones, in token order.
+    // ---- emit ------------------------------------------------------------------
+    // Ties at theta are ranked in token order only when some must be left out.
+    const bool rank_ties = ksel > 0 && eq_total != need_eq;
     uint64_t eqb[kPer];
+    if (rank_ties) {
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        eqb[i] = __builtin_amdgcn_ballot_w64(ksel > 0 && ((cand >> i) & 1u) && u[i] == theta);
-        if (lane == 0) runs[i * kWaves + wave] = (int)__builtin_popcountll(eqb[i]);
+        for (int i = 0; i < kPer; ++i) {
+            eqb[i] = __builtin_amdgcn_ballot_w64(((comp >> i) & 1u) && u[i] == theta);
+            if (lane == 0) runs[i * kWaves + wave] = (int)__builtin_popcountll(eqb[i]);
+        }
+        __syncthreads();
+        scan_runs(runs, scan_buf);
     }
-    __syncthreads();
-    scan_runs(runs, scan_buf);
-    uint32_t keep = 0;
+    // forced tokens (prefix, recent window) below N, the sure candidates, and
+    // the competing ones at or above theta (ties only as far as need_eq)
+    uint32_t valid = 0;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        const bool c = (cand >> i) & 1u;
-        const int j = tid + i * kThreads;
-        bool k;
-        if (j >= N)
-            k = false;
-        else if (!c)
-            k = true;  // forced prefix / recent window
-        else if (ksel <= 0)
-            k = false;
-        else if (u[i] > theta)
-            k = true;
-        else
-            k = u[i] == theta && runs[i * kWaves + wave] + rank_in_wave(eqb[i]) < need_eq;
-        if (k) keep |= 1u << i;
+    for (int i = 0; i < kPer; ++i) valid |= (tid + i * kThreads < N ? 1u : 0u) << i;
+    uint32_t keep = valid & ~pos_cand;
+    if (ksel > 0) {
+        keep |= sure;
+        const uint32_t wcomp = wave_or_u32(comp);
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            if (!((wcomp >> i) & 1u)) continue;  // wave-uniform
+            bool k = u[i] > theta;
+            if (u[i] == theta) k = !rank_ties || runs[i * kWaves + wave] + rank_in_wave(eqb[i]) < need_eq;
+            if (((comp >> i) & 1u) && k) keep |= 1u << i;
+        }
     }
-    __syncthreads();  // tie ranks read before the counts are reused
+    if (rank_ties) __syncthreads();  // tie ranks read before the counts are reused
     uint64_t kb[kPer];
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {

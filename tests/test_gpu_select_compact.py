@@ -25,6 +25,10 @@ def _scores(P, N, seed, kind):
         s[:, ::7] = -1.0
     elif kind == "wide":  # spans many binades, both signs, huge and tiny
         s = torch.randn(P, N, generator=g) * torch.exp(torch.randn(P, N, generator=g) * 20)
+    elif kind.startswith("cluster"):  # the threshold inside a tight cluster of n nearly equal scores
+        n = int(kind[7:])
+        s = -torch.rand(P, N, generator=g) * 12
+        s[:, 1:1 + n] = -1.5 - torch.rand(P, n, generator=g) * 1e-3
     elif kind == "minus-inf":
         s = -torch.rand(P, N, generator=g)
         s[:, ::3] = float("-inf")
@@ -45,6 +49,10 @@ TOPK = [
     (1, 1, 1, 8, 1, 0, "normal"),
     (2, 2, 65536, 8192, 128, 0, "normal"),  # the largest configuration's shape
     (16, 8, 32768, 4096, 32, 0, "ties"),    # the benchmark configuration's shape
+    (16, 8, 32768, 4096, 32, 0, "normal"),  # a few dozen candidates after the first digit
+    (4, 2, 32768, 4096, 32, 3, "cluster600"),   # hundreds of candidates, ranked directly
+    (4, 2, 32768, 4096, 32, 3, "cluster3000"),  # too many to rank: radix passes continue
+    (2, 2, 20000, 5000, 16, 0, "cluster1000"),
 ]
 
 
