@@ -5,11 +5,12 @@
 // kept is strictly ascending, so kept[i] >= i: a row only ever moves
 // towards the front.  Work items are segments of kSegRows destination rows;
 // each head's workgroups take their segment numbers from a per-head ticket,
-// so segments of a head start in order.  A segment first loads all of its source rows into
-// registers and publishes "read done"; before writing it waits for every
-// lower segment of the same head whose sources reach into its destination
-// rows (only lower segments can: a segment's sources lie at or after its
-// own first row).  Those segments hold lower tickets, have started, and
+// so segments of a head start in order.  A segment first loads all of its
+// source rows into registers and publishes "read done"; before writing it
+// waits for every lower segment of the same head whose source range meets
+// its destination rows (row x is read only by the segment holding the kept
+// index x, and kept[j] >= j puts that segment at or below this one).  With
+// a sparse selection that is about one segment, started long before.  Those segments hold lower tickets, have started, and
 // publish before they wait, so the waits always end.  Rows already in
 // place (kept[i] == i) are neither read nor written.
 //
@@ -98,11 +99,15 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
     __syncthreads();
     if (tid == 0) dev::st_flag(a.flags + (size_t)h * a.nseg + seg, 1);
     if (move) {
-        // Wait for lower segments whose last source row reaches our first row.
+        // Wait for the lower segments whose source rows [first, last] meet
+        // our destination rows [i0, i0 + rows): row x is read only by the
+        // segment holding the kept index x, which is at or below ours.
         if (tid < 64) {
             for (int sp = tid; sp < seg; sp += 64) {
+                const int first_src = kh[sp * kSegRows];
                 const int last_src = kh[min((sp + 1) * kSegRows, a.n_keep) - 1];
-                if (last_src >= i0) {
+                const bool meets = last_src >= i0 && first_src < i0 + rows;
+                if (meets) {
                     if (!dev::wait_flag(a.flags + (size_t)h * a.nseg + sp)) {
                         s_wait_ok = 0;
                         dev::raise_error(a.hdr, kErrCompactWait);
