@@ -56,6 +56,8 @@ def _load():
     lib.orc_topk.restype = _i
     lib.orc_compact.argtypes = [_i, _i, _i, _p, _p, _p]
     lib.orc_compact.restype = _i
+    lib.orc_compact_fill.argtypes = [_i, _i, _i, _i, _p, _p, _p, _p]
+    lib.orc_compact_fill.restype = _i
     lib.orc_fps.argtypes = [_i, _i, _i, _i, _p, _p, ctypes.c_double, _p, _p]
     lib.orc_fps.restype = _i
     lib.orc_evict_head.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p,
@@ -259,6 +261,32 @@ def compact(K, V, kept):
             if rc:
                 raise RuntimeError(f"orc_compact failed ({rc})")
     return k, v
+
+
+def compact_fill(K, V, kept, N: int):
+    """Hole-filling compaction on copies of K and V [B,Hkv,N_cap,D] with
+    kept [B,Hkv,n]: kept rows below n stay, the holes below n take the kept
+    rows at or above n in ascending order.  Returns (K', V' raw numpy,
+    src_of [B,Hkv,n] int32, moved [B,Hkv] rows moved)."""
+    lib = _load()
+    k, dt = _raw(K)
+    v, _ = _raw(V)
+    k = k.copy()
+    v = v.copy()
+    kp = np.ascontiguousarray(kept, dtype=np.int32)
+    B, Hkv, Ncap, D = k.shape
+    n = kp.shape[2]
+    es = 2 if dt == BF16 else 4
+    src_of = np.empty((B, Hkv, n), np.int32)
+    moved = np.empty((B, Hkv), np.int64)
+    for b in range(B):
+        for h in range(Hkv):
+            rc = lib.orc_compact_fill(es, D, N, n, _ptr(kp, (b * Hkv + h) * n), _ptr(k, (b * Hkv + h) * Ncap * D),
+                                      _ptr(v, (b * Hkv + h) * Ncap * D), _ptr(src_of, (b * Hkv + h) * n))
+            if rc < 0:
+                raise RuntimeError(f"orc_compact_fill failed ({rc})")
+            moved[b, h] = rc
+    return k, v, src_of, moved
 
 
 def evict(K, V, q_win, beacons, counts, N: int, budget: int, W: int, n_prefix: int = 0,

@@ -400,6 +400,40 @@ int orc_compact(int esize, int D, int n_keep, const int32_t* kept, void* Khead, 
     return 0;
 }
 
+/* ---- hole-filling compaction: another layout for the same kept set -----
+ *
+ * Algorithm 2 sorts the kept indices and gathers, so the cache stays in
+ * token order (orc_compact).  This variant leaves every kept row that lies
+ * below n_keep where it is and moves only the kept rows at or above n_keep:
+ * the m-th evicted position below n_keep (ascending) receives the m-th kept
+ * row at or above n_keep (ascending).  Rows [0, n_keep) then hold the kept
+ * set, not in token order; src_of[j] (j < n_keep) is the old position of
+ * the row now at j.  kept must be strictly ascending within [0, N).
+ * Returns the number of rows moved, or a negative error. */
+int orc_compact_fill(int esize, int D, int N, int n_keep, const int32_t* kept, void* Khead, void* Vhead,
+                     int32_t* src_of) {
+    size_t row = (size_t)esize * (size_t)D;
+    for (int i = 0; i < n_keep; ++i)
+        if (kept[i] < 0 || kept[i] >= N || (i > 0 && kept[i] <= kept[i - 1])) return -1;
+    unsigned char* in_place = (unsigned char*)calloc((size_t)(n_keep > 0 ? n_keep : 1), 1);
+    if (!in_place) return -2;
+    int c = 0;  /* kept rows already below n_keep: the first c entries of kept */
+    while (c < n_keep && kept[c] < n_keep) in_place[kept[c++]] = 1;
+    int m = 0;  /* holes filled so far */
+    for (int p = 0; p < n_keep; ++p) {
+        if (in_place[p]) {
+            src_of[p] = p;
+            continue;
+        }
+        const int src = kept[c + m++];
+        memcpy((unsigned char*)Khead + row * (size_t)p, (unsigned char*)Khead + row * (size_t)src, row);
+        memcpy((unsigned char*)Vhead + row * (size_t)p, (unsigned char*)Vhead + row * (size_t)src, row);
+        src_of[p] = src;
+    }
+    free(in_place);
+    return m;
+}
+
 /* ---- (a6) the whole eviction of one kv-head: (a2) -> (a3) -> (a4) -> (a5).
  * Returns the number of rows kept (or a negative error). */
 int orc_evict_head_ex(int dtype, int D, int N, int C, int G, int W, int budget, int n_prefix,
