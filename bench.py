@@ -299,8 +299,9 @@ def trace_measure(w, dev, B_max=4096, pool=16):
     prefill, then B_max - B_min decode steps run, the last of which evicts
     every layer back to B_min.  BeaconKV (16 beacon + 16 recent queries per
     head, Section 5.1) against RPC on the same kernels (32 recent queries,
-    no beacons; Table 1) and running-mean beacons (bkv_beacon_update every
-    step, 16 slots per query head).  Reported: the driver's wall time per step (host
+    no beacons; Table 1), running-mean beacons (bkv_beacon_update every
+    step, 16 slots per query head) and Initial+Recent (the prompt's first 16
+    queries per head frozen as beacons; Table 3).  Reported: the driver's wall time per step (host
     plus device, Python included) and the device time of the library calls
     per cycle from HIP events around each call."""
     import torch
@@ -323,7 +324,7 @@ def trace_measure(w, dev, B_max=4096, pool=16):
 
     res = {"config": {"layers": layers, "B": B, "Hq": Hq, "Hkv": Hkv, "D": D, "B_max": B_max, "B_min": B_min,
                       "steps_per_cycle": B_max - B_min}}
-    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("rpc", 0, 32)):
+    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("initial", 16, 16), ("rpc", 0, 32)):
         drv = PeriodicEviction(layers, B, Hq, Hkv, D, B_max, table, n_beacon=max(nb, 1), n_recent=nr, mode=mode,
                                device=dev, timing=True)
         Kp = torch.randn(LB, Hkv, B_min, D, generator=g, device=dev, dtype=torch.bfloat16)
@@ -363,7 +364,8 @@ def diagnostics_measure(w, dev, B=4, B_max=1024, cycles=8):
     in 4 groups; 2 % global queries, each aimed at one group; the rest
     local queries drifting slowly with the recent keys) runs through
     the periodic driver under Continual FPS beacons (16 + 16), running-mean
-    beacons (16 + 16) and recent queries only (32); per policy the planted
+    beacons (16 + 16), the prompt's first queries frozen (16 + 16) and
+    recent queries only (32); per policy the planted
     keys still cached after each eviction and the max-cosine coverage of
     the next 256 steps' queries by the observation set (Figure 6a's
     quantity), over all of them and over the global ones."""
@@ -378,7 +380,7 @@ def diagnostics_measure(w, dev, B=4, B_max=1024, cycles=8):
     res = {"config": dict(gen, B=B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, B_max=B_max, steps=T, prompt=B_max // 2,
                           horizon=256)}
     t0 = time.perf_counter()
-    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("rpc", 16, 32)):
+    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("initial", 16, 16), ("rpc", 16, 32)):
         r = diagnostics.run(tr, mode, B_max, n_beacon=nb, n_recent=nr, horizon=256)
         res[mode] = dict(diagnostics.summary(r), n_beacon=0 if mode == "rpc" else nb, n_recent=nr)
         print(f"# diagnostics {mode}: {res[mode]}", file=sys.stderr, flush=True)

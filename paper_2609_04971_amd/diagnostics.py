@@ -6,7 +6,8 @@ A trace from synth.revisit_trace plants "thought" keys that sparse global
 queries keep coming back to (the thought-revisiting tokens of Section 3.1),
 between local queries on recent keys.  Each policy runs the trace through
 the periodic eviction driver: BeaconKV's Continual FPS beacons ("beacon"),
-running-mean beacons ("ns", row a1) and recent queries only ("rpc").  At
+running-mean beacons ("ns", row a1), the prompt's first queries frozen
+("initial", Table 3's Initial+Recent) and recent queries only ("rpc").  At
 every eviction:
   * retention: the fraction of the planted keys still cached;
   * coverage: the mean, over the queries of the next `horizon` steps, of

@@ -28,6 +28,9 @@ buffer, no beacons (C = 0), the last n_recent queries before each eviction.
 mode "ns" keeps running-mean beacons instead of the FPS buffer: every
 step's pre-RoPE queries join the nearest of G * n_beacon slots per kv-head
 (bkv_beacon_update), and evictions score with those beacons as they stand.
+mode "initial" is the Initial+Recent baseline of Table 3: the first
+n_beacon queries of each query head (the prompt's) are frozen as its
+beacons for good, next to the same recent window.
 
 Everything that computes runs in the library's kernels; this module only
 slices the caller's tensors and appends rows to them (the writes a serving
@@ -49,8 +52,8 @@ class PeriodicEviction:
         rotated to the step at which eviction runs).  record keeps every
         call's inputs and outputs in `events`; timing brackets every library
         call with HIP events on the current stream, in `times`."""
-        if mode not in ("beacon", "rpc", "ns"):
-            raise ValueError("mode is 'beacon', 'rpc' or 'ns'")
+        if mode not in ("beacon", "rpc", "ns", "initial"):
+            raise ValueError("mode is 'beacon', 'rpc', 'ns' or 'initial'")
         if B_max % 8:
             raise ValueError("B_max must be a multiple of 8 (B_min = 7/8 B_max)")
         self.mode = mode
@@ -126,6 +129,12 @@ class PeriodicEviction:
             for t0 in range(0, T, tc):
                 qc = q_pre[:, :, t0:t0 + tc].contiguous()
                 self._call("beacon_update", lambda: bkv.beacon_update(self.dims, qc, self.beacons, self.counts))
+        if self.mode == "initial":
+            # every one of the first min(n_beacon, T) rows is picked (m >= n): the
+            # gather widens them into the beacon layout and sets their counts
+            self._call("beacon_widen", lambda: bkv.fps_gather(
+                q_pre, self.nb, n=min(self.nb, T), dst=self.beacons.view(self.LB, self.Hq, self.nb, self.D),
+                counts=self.counts.view(self.LB, self.Hq, self.nb)))
         if self.mode == "beacon":
             picks = torch.empty(self.LB, self.Hq, min(self.nb, T), dtype=torch.int32, device=K.device)
             self._call("fps_prefill", lambda: bkv.fps_gather(q_pre, self.nb, dst=self.obs, picks=picks))

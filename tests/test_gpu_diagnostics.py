@@ -40,7 +40,7 @@ def trace():
     return {k: (v.cuda() if torch.is_tensor(v) else v) for k, v in tr.items()}, tr
 
 
-@pytest.mark.parametrize("mode", ["beacon", "ns", "rpc"])
+@pytest.mark.parametrize("mode", ["beacon", "ns", "initial", "rpc"])
 def test_diagnostics_bookkeeping_and_metrics(trace, mode):
     tr, cpu = trace
     say(f"diagnostics {mode}: LB={LB} Hq={HQ} Hkv={HKV} D={D} B_max={B_MAX} T={T}")
@@ -86,6 +86,10 @@ def test_diagnostics_bookkeeping_and_metrics(trace, mode):
     if mode == "ns":
         # every query asked so far has joined one slot
         assert int(host(drv.counts).sum()) == LB * HQ * T
+    if mode == "initial":
+        # the first NB queries of every query head, frozen at prefill
+        want = q[:, :, :NB].reshape(LB, HKV, G * NB, D)
+        assert torch.equal(host(drv.beacons), want) and bool((host(drv.counts) == 1).all())
     say(f"  {diagnostics.summary(res)}")
 
 
@@ -96,7 +100,7 @@ def test_beacons_keep_the_revisited_keys():
     # baseline gets twice the recent queries, the same observation budget)
     tr = synth.revisit_trace(2, 32, 8, 128, 2048, seed=11, device="cuda")
     got = {}
-    for mode, nr in (("beacon", 16), ("ns", 16), ("rpc", 32)):
+    for mode, nr in (("beacon", 16), ("ns", 16), ("initial", 16), ("rpc", 32)):
         got[mode] = diagnostics.summary(diagnostics.run(tr, mode, 1024, n_beacon=16, n_recent=nr, horizon=256))
         say(f"{mode}: {got[mode]}")
     assert got["beacon"]["retention_mean"] > got["rpc"]["retention_mean"] + 0.1
