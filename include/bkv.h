@@ -183,6 +183,27 @@ bkv_status bkv_topk(const bkv_dims* d, const float* scores, int32_t* kept, void*
 bkv_status bkv_compact(const bkv_dims* d, void* K, void* V, const int32_t* kept, void* ws,
                        size_t ws_bytes, hipStream_t stream);
 
+/* Hole-filling compaction: another layout for the kept set of bkv_compact.
+ * For n = min(budget, N): every kept row below n stays where it is, and the
+ * m-th evicted position below n (ascending) receives the m-th kept row at
+ * or above n (ascending), bit for bit, so rows [0, n) of K and V hold the
+ * kept set, not in token order, and only the kept rows past n move.
+ * Algorithm 2 sorts and gathers (bkv_compact, order preserved); with the
+ * periodic eviction of Section 5.1 (B_max -> 7/8 B_max) this layout moves
+ * at most 1/8 of the cache instead of every row after the first evicted
+ * one.  The forcing rules of bkv_topk still hold across evictions: prefix
+ * rows are always kept and so never move, and tokens appended after an
+ * eviction stay at the end in order.  Scores do not depend on row order
+ * (RoPE is in the cached keys); top-k ties then go to the lower cache row.
+ *   kept    [B,Hkv,n] int32 read, strictly ascending within [0, N).
+ *   src_of  [B,Hkv,n] int32 written: the old row now at each row j < n
+ *           (j itself for rows that stayed).
+ * n <= 65536, else BKV_ERR_SHAPE.  A head whose kept indices are not
+ * ascending within [0, N) moves nothing (src_of = identity) and raises
+ * BKV_ERR_DEVICE.  Workspace: bkv_workspace_bytes(d, COMPACT). */
+bkv_status bkv_compact_fill(const bkv_dims* d, void* K, void* V, const int32_t* kept, int32_t* src_of,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* (a6) The whole eviction of one layer: bkv_score, bkv_topk, bkv_compact in
  * order on `stream`.  scores, row_lse and kept are optional outputs (NULL:
  * scores and kept live in the workspace).  Afterwards each head holds

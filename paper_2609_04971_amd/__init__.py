@@ -25,7 +25,7 @@ OP_BEACON_UPDATE, OP_SCORE, OP_TOPK, OP_COMPACT, OP_EVICT = range(5)
 EXPORTS = ("bkv_validate", "bkv_workspace_bytes", "bkv_workspace_init", "bkv_device_status",
            "bkv_beacon_update", "bkv_score", "bkv_topk", "bkv_compact", "bkv_evict",
            "bkv_score_ex", "bkv_evict_ex", "bkv_fps", "bkv_fps_gather", "bkv_status_string",
-           "bkv_abi_version")
+           "bkv_abi_version", "bkv_compact_fill")
 SCORE_MEAN, SCORE_CAUSAL = 1, 2
 
 
@@ -236,6 +236,18 @@ def compact(d: Dims, K, V, kept, ws):
                           _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
                           _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept"), wp, wn, _stream())
     _check(st, "bkv_compact")
+
+
+def compact_fill(d: Dims, K, V, kept, src_of, ws):
+    """Hole-filling compaction in place: kept rows below n stay, the holes
+    below n take the kept rows past n; src_of [B,Hkv,n] int32 receives the
+    old row now at each row."""
+    wp, wn = _ws(ws)
+    st = lib().bkv_compact_fill(ctypes.byref(d), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+                                _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
+                                _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept"),
+                                _ptr(src_of, (d.B, d.Hkv, d.n_keep), torch.int32, "src_of"), wp, wn, _stream())
+    _check(st, "bkv_compact_fill")
 
 
 def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row_lse=None, rope_cos=None,

@@ -211,6 +211,19 @@ bkv_status bkv_compact(const bkv_dims* d, void* K, void* V, const int32_t* kept,
     return map_hip(launch_compact(*d, L, K, V, kept, ws, stream));
 }
 
+bkv_status bkv_compact_fill(const bkv_dims* d, void* K, void* V, const int32_t* kept, int32_t* src_of, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+    bkv_status st = bkv_validate(d, BKV_OP_COMPACT);
+    if (st != BKV_OK) return st;
+    if (empty_batch(d) || d->N == 0) return BKV_OK;
+    if (!K || !V || !kept || !src_of) return BKV_ERR_INVALID;
+    if (!aligned16(K) || !aligned16(V)) return BKV_ERR_INVALID;
+    if ((d->N < d->budget ? d->N : d->budget) > kMaxFillKeep) return BKV_ERR_SHAPE;
+    const WsLayout L = ws_layout(*d);
+    if (!ws || ws_bytes < L.ctl_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
+    return map_hip(launch_compact_fill(*d, K, V, kept, src_of, ws, stream));
+}
+
 bkv_status bkv_evict(const bkv_dims* d, void* K, void* V, const void* q_win, const float* beacons,
                      const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
                      int32_t* kept, float* scores, float* row_lse, void* ws, size_t ws_bytes,

@@ -1,0 +1,162 @@
+// Hole-filling compaction for gfx950: rows [0, n) of each head end up
+// holding the kept set, but only the kept rows at or above n move.  A kept
+// row below n stays where it is; the m-th evicted position below n
+// (ascending) takes the m-th kept row at or above n (ascending).  The
+// order-preserving compaction of Algorithm 2 (Gather after Sort) shifts
+// every row after the first evicted one; this layout moves at most the
+// kept rows that lie past n, which after a periodic eviction of B_max -> 7/8
+// B_max (Section 5.1) is at most 1/8 of the cache.
+//
+// Sources lie at or above n and destinations below it, so no move can read
+// a row another move writes: the copy needs no ordering at all.  One
+// workgroup per head first writes src_of (the old position of the row each
+// position ends up with), then a grid of 64-row items copies the rows whose
+// src_of differs from their position.
+//
+// src_of: a bitmap of the kept positions below n goes to LDS; position p
+// is a hole of rank m = p - (kept positions below p), counted with a block
+// scan of the bitmap words' popcounts, and takes kept[c + m], c being the
+// number of kept rows below n.
+#include "device_common.h"
+#include "internal.h"
+
+namespace bkv {
+namespace {
+
+constexpr int kMapThreads = 1024;
+constexpr int kMapWaves = kMapThreads / 64;
+constexpr int kCopyThreads = 256;
+constexpr int kCopyRows = 64;
+
+// Exclusive scan of one int per thread over the block; buf holds kMapWaves ints.
+__device__ __forceinline__ int block_excl_scan(int v, int* buf) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) buf[wave] = x;
+    __syncthreads();
+    int before = x - v;
+    for (int w = 0; w < wave; ++w) before += buf[w];
+    __syncthreads();
+    return before;
+}
+
+__global__ __launch_bounds__(kMapThreads) void fill_map_kernel(const int32_t* __restrict__ kept,
+                                                               int32_t* __restrict__ src_of, int N, int n_keep,
+                                                               int P, int budget, int* hdr) {
+    __shared__ uint32_t bits[kMaxFillKeep / 32];
+    __shared__ int scan_buf[kMapWaves];
+    __shared__ int s_c, s_bad, s_ok;
+    const int h = blockIdx.x, tid = threadIdx.x;
+    const int32_t* kh = kept + (size_t)h * n_keep;
+    int32_t* so = src_of + (size_t)h * n_keep;
+    const int nw = (n_keep + 31) / 32;
+    for (int w = tid; w < nw; w += kMapThreads) bits[w] = 0u;
+    if (tid == 0) {
+        s_c = 0;
+        s_bad = 0;
+        const dev::u32x4 hd = *reinterpret_cast<const dev::u32x4*>(hdr);
+        s_ok = hd[kHdrMagic] == kWsMagic && (int)hd[kHdrP] == P && (int)hd[kHdrBudget] == budget;
+        if (!s_ok) dev::raise_error(hdr, kErrStamp);
+    }
+    __syncthreads();
+    int below = 0;  // kept positions below n seen by this thread
+    for (int i = tid; i < n_keep; i += kMapThreads) {
+        const int k = kh[i];
+        if (k < 0 || k >= N || (i > 0 && k <= kh[i - 1])) s_bad = 1;  // benign race: any writer stores 1
+        if (k >= 0 && k < n_keep) {
+            atomicOr(&bits[k >> 5], 1u << (k & 31));
+            ++below;
+        }
+    }
+    if (below) atomicAdd(&s_c, below);
+    __syncthreads();
+    if (s_bad && tid == 0) dev::raise_error(hdr, kErrBadIndex);
+    if (s_bad || !s_ok) {  // move nothing
+        for (int p = tid; p < n_keep; p += kMapThreads) so[p] = p;
+        return;
+    }
+    const int c = s_c;
+    // thread t walks the bitmap words [w0, w1), in order
+    const int wpt = (nw + kMapThreads - 1) / kMapThreads;
+    const int w0 = min(tid * wpt, nw), w1 = min(w0 + wpt, nw);
+    int mine = 0;
+    for (int w = w0; w < w1; ++w) mine += __builtin_popcount(bits[w]);
+    int kept_below = block_excl_scan(mine, scan_buf);  // kept positions below word w0
+    for (int w = w0; w < w1; ++w) {
+        const uint32_t b = bits[w];
+        for (int i = 0; i < 32; ++i) {
+            const int p = w * 32 + i;
+            if (p >= n_keep) break;
+            if ((b >> i) & 1u) {
+                so[p] = p;
+                ++kept_below;
+            } else {
+                so[p] = kh[c + (p - kept_below)];  // hole of rank p - kept_below
+            }
+        }
+    }
+}
+
+// RB = row bytes; VPR = 16-byte vectors per row.  Item (head, chunk) moves
+// the rows of positions [64 chunk, 64 chunk + 64) whose source differs.
+template <int RB>
+__global__ __launch_bounds__(kCopyThreads) void fill_copy_kernel(char* K, char* V, const int32_t* __restrict__ src_of,
+                                                                 int n_keep, int nchunk, size_t head_stride) {
+    constexpr int VPR = RB / 16;
+    constexpr int NV = 2 * kCopyRows * VPR / kCopyThreads;  // 16-byte vectors per thread (K and V)
+    __shared__ int s_src[kCopyRows];
+    const int h = blockIdx.x / nchunk, ch = blockIdx.x - h * nchunk;
+    const int j0 = ch * kCopyRows, rows = min(kCopyRows, n_keep - j0);
+    const int tid = threadIdx.x;
+    if (tid < rows) s_src[tid] = src_of[(size_t)h * n_keep + j0 + tid];
+    __syncthreads();
+    char* Kh = K + (size_t)h * head_stride;
+    char* Vh = V + (size_t)h * head_stride;
+    dev::u32x4 buf[NV];
+    dev::static_for<NV>([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        const int e = tid + k * kCopyThreads;
+        const int which = e / (kCopyRows * VPR);
+        const int r = (e / VPR) % kCopyRows, v = e % VPR;
+        if (r < rows && s_src[r] != j0 + r)
+            buf[k] = reinterpret_cast<const dev::u32x4*>((which ? Vh : Kh) + (size_t)s_src[r] * RB)[v];
+    });
+    dev::static_for<NV>([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        const int e = tid + k * kCopyThreads;
+        const int which = e / (kCopyRows * VPR);
+        const int r = (e / VPR) % kCopyRows, v = e % VPR;
+        if (r < rows && s_src[r] != j0 + r)
+            reinterpret_cast<dev::u32x4*>((which ? Vh : Kh) + (size_t)(j0 + r) * RB)[v] = buf[k];
+    });
+}
+
+}  // namespace
+
+hipError_t launch_compact_fill(const bkv_dims& d, void* K, void* V, const int32_t* kept, int32_t* src_of, void* ws,
+                               hipStream_t s) {
+    const int P = d.B * d.Hkv;
+    const int n_keep = d.N < d.budget ? d.N : d.budget;
+    if (P == 0 || n_keep == 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_map_kernel, dim3(P), dim3(kMapThreads), 0, s, kept, src_of, d.N, n_keep, P, d.budget,
+                       static_cast<int*>(ws));
+    const int nchunk = (n_keep + kCopyRows - 1) / kCopyRows;
+    const int es = d.dtype == BKV_BF16 ? 2 : 4;
+    const int rb = d.D * es;
+    const size_t hs = (size_t)d.N_cap * rb;
+    char* k = static_cast<char*>(K);
+    char* v = static_cast<char*>(V);
+    switch (rb) {
+        case 128: hipLaunchKernelGGL(fill_copy_kernel<128>, dim3(P * nchunk), dim3(kCopyThreads), 0, s, k, v, src_of, n_keep, nchunk, hs); break;
+        case 256: hipLaunchKernelGGL(fill_copy_kernel<256>, dim3(P * nchunk), dim3(kCopyThreads), 0, s, k, v, src_of, n_keep, nchunk, hs); break;
+        default: hipLaunchKernelGGL(fill_copy_kernel<512>, dim3(P * nchunk), dim3(kCopyThreads), 0, s, k, v, src_of, n_keep, nchunk, hs); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace bkv

@@ -40,6 +40,7 @@ enum HeadWord : int {
 enum DevErr : int { kErrScoreWait = 1, kErrCompactWait = 2, kErrStamp = 4, kErrBadIndex = 8 };
 
 constexpr int kSegRows = 64;  // compaction rows per work item
+constexpr int kMaxFillKeep = 65536;  // hole-filling compaction: kept rows per head at most (LDS bitmap)
 
 // Per-head row metadata written before scoring: word 0 = number of occupied
 // beacon slots, words kMetaAct.. = those slots, ascending.
@@ -77,6 +78,8 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
                         void* ws, hipStream_t s);
 
 hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hipStream_t s);
+hipError_t launch_compact_fill(const bkv_dims& d, void* K, void* V, const int32_t* kept, int32_t* src_of, void* ws,
+                               hipStream_t s);
 
 hipError_t launch_compact(const bkv_dims& d, const WsLayout& L, void* K, void* V,
                           const int32_t* kept, void* ws, hipStream_t s);

@@ -203,3 +203,15 @@ def test_score_ex_rejects_unknown_flags_and_keeps_rules():
                                 None, 0, None) == bkv.ERR_SHAPE
         assert lib.bkv_score_ex(ctypes.byref(good(N=0)), f, None, None, None, None, None, None, 0.0, None, None,
                                 None, 0, None) == bkv.OK
+
+
+def test_compact_fill_rejects_before_launch():
+    lib = bkv.lib()
+    d = good()
+    r = ctypes.byref(d)
+    assert lib.bkv_compact_fill(r, None, None, None, None, None, 0, None) == bkv.ERR_INVALID
+    big = good(N=70000, N_cap=70000, budget=66000)  # more kept rows per head than the LDS bitmap holds
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: the shape is rejected first
+    assert lib.bkv_compact_fill(ctypes.byref(big), fake, fake, fake, fake, None, 0, None) == bkv.ERR_SHAPE
+    empty = good(B=0)
+    assert lib.bkv_compact_fill(ctypes.byref(empty), None, None, None, None, None, 0, None) == bkv.OK

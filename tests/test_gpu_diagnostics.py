@@ -87,9 +87,14 @@ def test_diagnostics_bookkeeping_and_metrics(trace, mode):
         # every query asked so far has joined one slot
         assert int(host(drv.counts).sum()) == LB * HQ * T
     if mode == "initial":
-        # the first NB queries of every query head, frozen at prefill
-        want = q[:, :, :NB].reshape(LB, HKV, G * NB, D)
-        assert torch.equal(host(drv.beacons), want) and bool((host(drv.counts) == 1).all())
+        # the first NB queries of every query head, frozen at prefill (in
+        # the gather's selection order: compared as a permutation)
+        bc = host(drv.beacons).view(LB, HQ, NB, D)
+        for b in range(LB):
+            for hq in range(HQ):
+                hit = (bc[b, hq][:, None, :] == q[b, hq, :NB][None, :, :]).all(-1)  # [beacon, query]
+                assert sorted(hit.float().argmax(1).tolist()) == list(range(NB)) and bool(hit.any(1).all())
+        assert bool((host(drv.counts) == 1).all())
     say(f"  {diagnostics.summary(res)}")
 
 
