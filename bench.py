@@ -301,7 +301,9 @@ def trace_measure(w, dev, B_max=4096, pool=16):
     head, Section 5.1) against RPC on the same kernels (32 recent queries,
     no beacons; Table 1), running-mean beacons (bkv_beacon_update every
     step, 16 slots per query head) and Initial+Recent (the prompt's first 16
-    queries per head frozen as beacons; Table 3).  Reported: the driver's wall time per step (host
+    queries per head frozen as beacons; Table 3); and BeaconKV with the
+    hole-filling compaction (bkv_compact_fill: only the kept rows past B_min
+    move) in place of the order-preserving one.  Reported: the driver's wall time per step (host
     plus device, Python included) and the device time of the library calls
     per cycle from HIP events around each call."""
     import torch
@@ -324,9 +326,12 @@ def trace_measure(w, dev, B_max=4096, pool=16):
 
     res = {"config": {"layers": layers, "B": B, "Hq": Hq, "Hkv": Hkv, "D": D, "B_max": B_max, "B_min": B_min,
                       "steps_per_cycle": B_max - B_min}}
-    for mode, nb, nr in (("beacon", 16, 16), ("ns", 16, 16), ("initial", 16, 16), ("rpc", 0, 32)):
+    runs = (("beacon", 16, 16, "order"), ("beacon-fill", 16, 16, "fill"), ("ns", 16, 16, "order"),
+            ("initial", 16, 16, "order"), ("rpc", 0, 32, "order"))
+    for name, nb, nr, compaction in runs:
+        mode = name.split("-")[0]
         drv = PeriodicEviction(layers, B, Hq, Hkv, D, B_max, table, n_beacon=max(nb, 1), n_recent=nr, mode=mode,
-                               device=dev, timing=True)
+                               device=dev, timing=True, compaction=compaction)
         Kp = torch.randn(LB, Hkv, B_min, D, generator=g, device=dev, dtype=torch.bfloat16)
         Vp = torch.randn_like(Kp)
         qp = synth.query_stream(w.with_(B=LB), B_min, seed=5, device=dev)
@@ -350,7 +355,10 @@ def trace_measure(w, dev, B_max=4096, pool=16):
         for kind, e0, e1 in drv.times:
             per_kind[kind] = per_kind.get(kind, 0.0) + e0.elapsed_time(e1) * 1e3
         dev_us = sum(per_kind.values())
-        res[mode] = {"n_beacon": nb, "n_recent": nr, "steps": n, "wall_us_per_step": round(wall * 1e6 / n, 1),
+        ar = torch.arange(B_min, device=dev, dtype=torch.int32)
+        moved = float((drv.kept != ar).sum(-1).float().mean())  # rows the eviction moved, per kv-head
+        res[name] = {"n_beacon": nb, "n_recent": nr, "compaction": compaction, "steps": n,
+                     "rows_moved_per_head": round(moved, 1), "wall_us_per_step": round(wall * 1e6 / n, 1),
                      "library_us_per_cycle": {k: round(v, 1) for k, v in per_kind.items()},
                      "library_us_per_step": round(dev_us / n, 2)}
         del drv, kk, vv, qq

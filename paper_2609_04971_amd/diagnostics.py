@@ -55,7 +55,7 @@ def _identity_rope(D, device):
 
 
 def run(trace, mode: str, B_max: int, n_beacon: int = 16, n_recent: int = 16, prompt: int | None = None,
-        horizon: int = 256, record: bool = False):
+        horizon: int = 256, record: bool = False, compaction: str = "order"):
     """Run `trace` (synth.revisit_trace, on the GPU) through the periodic
     driver with policy `mode`.  Returns per-eviction retention and coverage
     (and, with record, the per-eviction observation sets, future queries
@@ -66,7 +66,7 @@ def run(trace, mode: str, B_max: int, n_beacon: int = 16, n_recent: int = 16, pr
     G = Hq // Hkv
     T0 = B_max // 2 if prompt is None else prompt
     drv = PeriodicEviction(1, LB, Hq, Hkv, D, B_max, _identity_rope(D, K.device), n_beacon=n_beacon,
-                           n_recent=n_recent, mode=mode, device=K.device)
+                           n_recent=n_recent, mode=mode, device=K.device, compaction=compaction)
     drv.prefill(K[:, :, :T0].contiguous(), V[:, :, :T0].contiguous(), q[:, :, :T0].contiguous())
     pos = torch.arange(T0, device=K.device).view(1, 1, T0).expand(LB, Hkv, T0).clone()
     out = {"retention": [], "coverage": [], "coverage_global": [], "steps": []}

@@ -32,6 +32,13 @@ mode "initial" is the Initial+Recent baseline of Table 3: the first
 n_beacon queries of each query head (the prompt's) are frozen as its
 beacons for good, next to the same recent window.
 
+compaction "fill" evicts with bkv_score, bkv_topk and bkv_compact_fill
+instead of bkv_evict_ex: the cache keeps the same rows but only the kept
+rows past B_min move (into the evicted rows below it), so rows are no
+longer in token order; `kept` then holds, for each row, the row it came
+from (what bkv_compact_fill calls src_of), which is also what `kept` means
+for the order-preserving compaction.
+
 Everything that computes runs in the library's kernels; this module only
 slices the caller's tensors and appends rows to them (the writes a serving
 engine makes to its own cache).
@@ -46,7 +53,7 @@ import paper_2609_04971_amd as bkv
 class PeriodicEviction:
     def __init__(self, layers: int, B: int, Hq: int, Hkv: int, D: int, B_max: int, rope_table, n_beacon: int = 16,
                  n_recent: int = 16, n_prefix: int = 0, mode: str = "beacon", dtype=torch.bfloat16,
-                 device="cuda", record: bool = False, timing: bool = False):
+                 device="cuda", record: bool = False, timing: bool = False, compaction: str = "order"):
         """rope_table(t) -> (cos, sin), fp32 [D/2] device tensors of the
         model's rotate-half RoPE at absolute position t (the beacons are
         rotated to the step at which eviction runs).  record keeps every
@@ -56,6 +63,9 @@ class PeriodicEviction:
             raise ValueError("mode is 'beacon', 'rpc', 'ns' or 'initial'")
         if B_max % 8:
             raise ValueError("B_max must be a multiple of 8 (B_min = 7/8 B_max)")
+        if compaction not in ("order", "fill"):
+            raise ValueError("compaction is 'order' or 'fill'")
+        self.compaction = compaction
         self.mode = mode
         self.LB, self.Hq, self.Hkv, self.D = layers * B, Hq, Hkv, D
         self.G = Hq // Hkv
@@ -85,6 +95,7 @@ class PeriodicEviction:
                              budget=self.B_min, n_prefix=n_prefix, dtype="bf16" if dt == torch.bfloat16 else "fp32")
         self.ws = bkv.workspace(self.dims, bkv.OP_EVICT, device=dev)
         self.kept = torch.empty(LB, Hkv, self.B_min, dtype=torch.int32, device=dev)
+        self.sel = torch.empty_like(self.kept) if compaction == "fill" else None  # top-k output before filling
         self.scores = torch.empty(LB, Hkv, B_max, dtype=torch.float32, device=dev)
         self.events = []  # (kind, details) of the calls made, when recording
         self.timing = timing
@@ -178,8 +189,17 @@ class PeriodicEviction:
     def _evict(self):
         rc, rs = self.rope_table(self.t - 1)  # beacons rotated to the current step
         pre = (self.K.clone(), self.V.clone()) if self.record else None
-        self._call("evict", lambda: bkv.evict(self.dims, self.K, self.V, self.recent_rope, self.beacons, self.counts,
-                                              self.ws, kept=self.kept, scores=self.scores, rope_cos=rc, rope_sin=rs))
+        if self.compaction == "order":
+            self._call("evict", lambda: bkv.evict(self.dims, self.K, self.V, self.recent_rope, self.beacons,
+                                                  self.counts, self.ws, kept=self.kept, scores=self.scores,
+                                                  rope_cos=rc, rope_sin=rs))
+        else:
+            def evict_fill():
+                bkv.score(self.dims, self.K, self.recent_rope, self.beacons, self.counts, self.scores, self.ws,
+                          rope_cos=rc, rope_sin=rs)
+                bkv.topk(self.dims, self.scores, self.sel)
+                bkv.compact_fill(self.dims, self.K, self.V, self.sel, self.kept, self.ws)
+            self._call("evict", evict_fill)
         self._log("evict", before=pre, q_win=self.recent_rope.clone() if self.record else None,
                   beacons=self.beacons.clone() if self.record else None,
                   counts=self.counts.clone() if self.record else None, rope=(rc, rs), kept=self.kept.clone(),

@@ -3,7 +3,8 @@ periodic driver in each policy (Continual FPS beacons, running-mean beacons,
 recent queries only).  The test checks the bookkeeping the metrics rest on
 and recomputes the metrics in numpy:
   * the cached positions the diagnostics track name the rows the driver's
-    cache really holds (K bit-exact against the trace at those positions);
+    cache really holds (K bit-exact against the trace at those positions),
+    also with the hole-filling compaction, whose rows leave token order;
   * the recent part of every observation set is the last n_recent queries of
     each query head; Continual FPS beacons are queries the head asked before
     the window; running-mean counts add up to every query asked so far;
@@ -40,12 +41,16 @@ def trace():
     return {k: (v.cuda() if torch.is_tensor(v) else v) for k, v in tr.items()}, tr
 
 
-@pytest.mark.parametrize("mode", ["beacon", "ns", "initial", "rpc"])
-def test_diagnostics_bookkeeping_and_metrics(trace, mode):
+@pytest.mark.parametrize("mode,compaction", [("beacon", "order"), ("ns", "order"), ("initial", "order"),
+                                             ("rpc", "order"), ("beacon", "fill")])
+def test_diagnostics_bookkeeping_and_metrics(trace, mode, compaction):
+    # with compaction "fill" the cache is no longer in token order: the
+    # tracked positions follow the rows through bkv_compact_fill's src_of
     tr, cpu = trace
-    say(f"diagnostics {mode}: LB={LB} Hq={HQ} Hkv={HKV} D={D} B_max={B_MAX} T={T}")
+    say(f"diagnostics {mode} ({compaction}): LB={LB} Hq={HQ} Hkv={HKV} D={D} B_max={B_MAX} T={T}")
     nr = 2 * NR if mode == "rpc" else NR
-    res = diagnostics.run(tr, mode, B_MAX, n_beacon=NB, n_recent=nr, prompt=T0, horizon=HORIZON, record=True)
+    res = diagnostics.run(tr, mode, B_MAX, n_beacon=NB, n_recent=nr, prompt=T0, horizon=HORIZON, record=True,
+                          compaction=compaction)
     drv = res["driver"]
     assert res["steps"] == [127, 143, 159, 175, 191]
     assert np.isnan(res["coverage"][-1]) and not np.isnan(res["coverage"][:-1]).any()
