@@ -193,9 +193,12 @@ __global__ __launch_bounds__(64) void fps_gram_kernel(const T* src, int src_rows
     const float inv = live ? inv_norm(G[lane * kLdg + lane]) : 0.f;
 
     // first pick: argmin of the summed cosines of row `lane` (avg times n)
+    // (a compile-time bound with a wave-uniform test: the cross-lane read
+    // keeps a loop with a run-time trip count from being unrolled)
     float S = 0.f;
-#pragma unroll 8
-    for (int j = 0; j < n; ++j) S = fmaf(G[j * kLdg + lane], lane_value(inv, j), S);
+#pragma unroll
+    for (int j = 0; j < 16 * NB; ++j)
+        if (j < n) S = fmaf(G[j * kLdg + lane], lane_value(inv, j), S);
     S *= inv;
     bool done = !live;
     int mypick = 0;  // lane k keeps pick k
