@@ -79,6 +79,7 @@ def parse():
     ap.add_argument("--no-fps", action="store_true", help="skip the Continual FPS and scoring-option timings")
     ap.add_argument("--no-trace", action="store_true", help="skip the periodic-eviction cycle timing")
     ap.add_argument("--no-diag", action="store_true", help="skip the synthetic quality diagnostics")
+    ap.add_argument("--no-configs", action="store_true", help="skip the eviction timing of the other workloads")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -213,6 +214,8 @@ def main():
         out["continual_fps"] = fps_measure(w, dev)
     if not args.no_trace:
         out["periodic_eviction"] = trace_measure(w, dev)
+    if not args.no_configs:
+        out["configs"] = configs_measure(dev)
     if not args.no_diag:
         out["diagnostics"] = diagnostics_measure(w, dev)
     if not args.no_cpu_baseline:
@@ -362,6 +365,69 @@ def trace_measure(w, dev, B_max=4096, pool=16):
                      "library_us_per_cycle": {k: round(v, 1) for k, v in per_kind.items()},
                      "library_us_per_step": round(dev_us / n, 2)}
         del drv, kk, vv, qq
+        torch.cuda.empty_cache()
+    return res
+
+
+def configs_measure(dev, reps=5):
+    """Eviction latency of one layer (bkv_evict: score, top-k, compaction) on
+    each workload shape besides the benchmark's cold 32K layer: the small
+    fp32 case, the 4K layer, the steady-state eviction of the benchmark's
+    layer (4224 -> 4096 tokens, the 128-step cadence; also with the
+    hole-filling compaction), the GQA-7 16K layer and the 64K layer.  Each eviction runs on a fresh copy of the generated
+    layer (the copy is not timed); the median of `reps` is reported with the
+    throughput P * N / t and the score launch's share."""
+    import torch
+
+    import paper_2609_04971_amd as bkv
+    from paper_2609_04971_amd import synth
+
+    steady = synth.QWEN3_4B_32K.with_(N=4224)
+    shapes = [("tiny-fp32-N512", synth.TINY_FP32, False), ("qwen3-4b-layer-N4096", synth.QWEN3_4B_4K, False),
+              ("qwen3-4b-steady-N4224-to-4096", steady, False),
+              ("qwen3-4b-steady-N4224-to-4096-holefill", steady, True),
+              ("qwen2.5-7b-N16384-gqa7", synth.QWEN25_7B_16K, False), ("llama-8b-N65536", synth.LLAMA8B_64K, False)]
+    res = {}
+    for name, w, fill in shapes:
+        d = bkv.dims(B=w.B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, N=w.N, W=w.W, C=w.C, budget=w.budget, dtype=w.dtype)
+        x = synth.make_layer(w, seed=7, device=dev)
+        K0, V0 = x["K"].clone(), x["V"].clone()
+        ws = bkv.workspace(d, bkv.OP_EVICT)
+        kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device=dev)
+        scores = torch.empty(d.B, d.Hkv, d.N, device=dev)
+        src_of = torch.empty_like(kept) if fill else None
+        t_ev, t_sc = [], []
+        for r in range(reps + 1):
+            x["K"].copy_(K0)
+            x["V"].copy_(V0)
+            torch.cuda.synchronize()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record()
+            bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+                      rope_sin=x["rope_sin"])
+            e[1].record()
+            bkv.topk(d, scores, kept)
+            if fill:
+                bkv.compact_fill(d, x["K"], x["V"], kept, src_of, ws)
+            else:
+                bkv.compact(d, x["K"], x["V"], kept, ws)
+            e[2].record()
+            torch.cuda.synchronize()
+            if r:  # the first is a warm-up
+                t_ev.append(e[0].elapsed_time(e[2]) * 1e3)
+                t_sc.append(e[0].elapsed_time(e[1]) * 1e3)
+        assert bkv.device_status(ws) == bkv.OK
+        t = sorted(t_ev)[len(t_ev) // 2]
+        ts = sorted(t_sc)[len(t_sc) // 2]
+        es = 2 if w.dtype == "bf16" else 4
+        kbytes = d.B * d.Hkv * w.N * (w.D * es + 4)
+        res[name] = {"B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "N": w.N, "W": w.W, "C": w.C,
+                     "budget": w.budget, "R": w.C + w.G * w.W, "dtype": w.dtype,
+                     "compaction": "hole-filling" if fill else "order-preserving",
+                     "eviction_latency_us": round(t, 1), "rows_per_s": round(d.B * d.Hkv * w.N / (t * 1e-6), 1),
+                     "score_us": round(ts, 1), "score_frac_of_hbm_peak": round(kbytes / (ts * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+        print(f"# config {name}: eviction {t:.1f} us, score {ts:.1f} us", file=sys.stderr, flush=True)
+        del x, K0, V0, ws, kept, scores
         torch.cuda.empty_cache()
     return res
 
