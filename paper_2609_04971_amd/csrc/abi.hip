@@ -49,11 +49,22 @@ WsLayout ws_layout(const bkv_dims& d) {
     L.ctl_end = off;
     // data (depends on N, W, C as well)
     const int R = d.C + G * d.W;
-    L.R_pad_max = (R + 15) / 16 * 16;
+    const int tiles = (R + 15) / 16;
+    L.rtg = 0;
+    L.R_pad_max = tiles * 16;
+    if (d.dtype == BKV_BF16 && tiles <= kFastTiles * kFastRowGroups) {
+        // fast path: rows in equal groups of at most kFastTiles tiles, padded
+        // with rows that never win
+        const int nrg = max(1, (tiles + kFastTiles - 1) / kFastTiles);
+        L.rtg = max(1, (tiles + nrg - 1) / nrg);
+        L.R_pad_max = nrg * L.rtg * 16;
+    }
     // key chunk per score work item: 1024 keys once there are enough chunks
-    // to fill the machine several times over, else 256
+    // to fill the machine several times over, or when the rows span several
+    // row groups (each group streams the chunk again, so short chunks would
+    // spend their time on per-group set-up); else 256
     const long long big = (long long)P * ((d.N + 1023) / 1024);
-    L.kgn = big >= 2048 ? 4 : 1;
+    L.kgn = (big >= 2048 || tiles > kFastTiles) ? 4 : 1;
     L.key_chunk = 256 * L.kgn;
     L.nch = (d.N + L.key_chunk - 1) / L.key_chunk;
     L.part_m = off;

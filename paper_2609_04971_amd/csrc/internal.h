@@ -62,7 +62,13 @@ struct WsLayout {
     size_t kept;            // evict: kept indices when the caller passes none [P][budget]
     size_t evict_end;
     int P, nseg, R_pad_max, nch, kgn, key_chunk;
+    int rtg;  // score fast path: row tiles (16 rows) per row group; 0 selects the generic path
 };
+
+// The score fast path (bf16) holds the rows of one row group in registers:
+// at most kFastTiles tiles per group and kFastRowGroups groups.
+constexpr int kFastTiles = 9;
+constexpr int kFastRowGroups = 8;
 
 WsLayout ws_layout(const bkv_dims& d);
 

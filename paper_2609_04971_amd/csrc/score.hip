@@ -584,12 +584,17 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
         final_item<T, D, KGN>(a, h, s_ticket - a.nch, sm, &s_flag);
 }
 
-// ---- fast path: bf16 cache, at most 144 observation rows -----------------
+// ---- fast path: bf16 cache, rows in groups of at most 144 ------------------
 //
 // A small kernel first writes each head's observation rows to the workspace
 // in MFMA operand order, so that a work item loads them straight into
-// registers with coalesced 16-byte loads, issued before its ticket returns;
-// they stay in registers for the whole item.  Key tiles are staged through
+// registers with coalesced 16-byte loads.  When all rows fit in one group of
+// at most 144 (9 tiles) they are loaded before the item's ticket returns and
+// stay in registers for the whole item.  Wider heads (up to 8 groups) split
+// the rows into equal groups: an item takes them one after the other,
+// streaming its key chunk again for each (from L2 or the memory-side cache);
+// S items store each group's row statistics, F items keep each key's max
+// (or sum) over the groups so far in LDS and write it after the last.  Key tiles are staged through
 // LDS with coalesced global_load_lds_dwordx4 (direct to LDS, no registers),
 // double-buffered per wave so the next group of 32 keys is in flight while
 // this one is computed; a 16-lane ds_read_b128 of a staged tile is
@@ -600,7 +605,7 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(Args a) {
 // unrolled by two, so every LDS read names one stage; the compiler then
 // waits only for the loads into that stage, not for the group in flight
 // into the other one.
-constexpr int kFRT = 9;   // at most this many 16-row tiles
+constexpr int kFRT = kFastTiles;  // at most this many 16-row tiles per row group
 constexpr int kFKG = 32;  // keys per group: two 16-key tiles
 
 template <int D>
@@ -618,6 +623,8 @@ struct alignas(16) StageBuf {
     uint16_t k[kWaves][KeyStage<D>::ELEMS];
 };
 
+constexpr int kMaxKeyChunk = 1024;  // keys per work item at most
+
 struct alignas(16) FastSmem {
     union {
         struct {
@@ -627,12 +634,14 @@ struct alignas(16) FastSmem {
         float nlse[kFRT * 16];  // F items: -lse of each row (raw-dot units)
     } v;
     int lim[kFRT * 16];         // last key each row sees (KeyMask::limit)
+    float kacc[kMaxKeyChunk];   // F items with several row groups: each key's result so far
 };
 
-// Each row's key limit into LDS, for the groups that mask (key, row) pairs.
+// Each row's key limit into LDS (rows r0 .. r0 + 16 RT - 1), for the groups
+// that mask (key, row) pairs.
 template <int RT>
-__device__ __forceinline__ void fill_limits(const KeyMask& mk, int* lim) {
-    for (int r = threadIdx.x; r < RT * 16; r += kThreads) lim[r] = mk.limit(r);
+__device__ __forceinline__ void fill_limits(const KeyMask& mk, int r0, int* lim) {
+    for (int r = threadIdx.x; r < RT * 16; r += kThreads) lim[r] = mk.limit(r0 + r);
 }
 
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
@@ -654,23 +663,30 @@ __global__ __launch_bounds__(kThreads) void rows_kernel(Args a) {
     const int h = blockIdx.x, tid = threadIdx.x;
     reset_head_control(a, h);
     active_slots(a, h, act, &nact);
-    build_rows<uint16_t, D, LD>(a, h, 0, a.R_pad_max, act, nact, y);
-    __syncthreads();
-    dev::u32x4* out = reinterpret_cast<dev::u32x4*>(a.rows) + (size_t)h * a.R_pad_max * D / 8;
-    const int n = a.R_pad_max / 16 * NV * 64;
-    for (int i = tid; i < n; i += kThreads) {
-        const int lane = i & 63, v = (i >> 6) % NV, rt = (i >> 6) / NV;
-        out[i] = *reinterpret_cast<const dev::u32x4*>(y + (rt * 16 + (lane & 15)) * LD + (4 * v + (lane >> 4)) * 8);
+    // up to 144 rows at a time through LDS
+    for (int r0 = 0; r0 < a.R_pad_max; r0 += kFRT * 16) {
+        const int nr = min(kFRT * 16, a.R_pad_max - r0);
+        build_rows<uint16_t, D, LD>(a, h, r0, nr, act, nact, y);
+        __syncthreads();
+        dev::u32x4* out = reinterpret_cast<dev::u32x4*>(a.rows) + ((size_t)h * a.R_pad_max + r0) * D / 8;
+        const int n = nr / 16 * NV * 64;
+        for (int i = tid; i < n; i += kThreads) {
+            const int lane = i & 63, v = (i >> 6) % NV, rt = (i >> 6) / NV;
+            out[i] = *reinterpret_cast<const dev::u32x4*>(y + (rt * 16 + (lane & 15)) * LD + (4 * v + (lane >> 4)) * 8);
+        }
+        __syncthreads();
     }
     int* meta = a.rmeta + (size_t)h * kMetaWords;
     if (tid == 0) meta[0] = nact;
     for (int c = tid; c < nact; c += kThreads) meta[kMetaAct + c] = act[c];
 }
 
+// Row group rg (rows 16 RT rg .. 16 RT (rg + 1) - 1) of head h into registers.
 template <int D, int RT>
-__device__ __forceinline__ void load_rows(const Args& a, int h, Op<uint16_t, D>* yr, int lane) {
+__device__ __forceinline__ void load_rows(const Args& a, int h, int rg, Op<uint16_t, D>* yr, int lane) {
     constexpr int NV = Op<uint16_t, D>::NV;
-    const dev::u32x4* src = reinterpret_cast<const dev::u32x4*>(a.rows) + (size_t)h * RT * 16 * D / 8 + lane;
+    const dev::u32x4* src =
+        reinterpret_cast<const dev::u32x4*>(a.rows) + ((size_t)h * a.R_pad_max + (size_t)rg * RT * 16) * D / 8 + lane;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -778,9 +794,14 @@ __device__ __forceinline__ void stats_group(const uint16_t* st, int kb, const in
 // Pipelined like stats_group; each tile's -lse seed is read from LDS two
 // tiles ahead (re-read every group through an offset the compiler cannot
 // hoist: kept for the whole item these would hold 4 * RT registers).
+// Row-group phase of an F item: its only group, or the first, a middle or
+// the last of several (then each key's result is combined in kacc).
+enum RowPhase : int { kOnlyGroup = 0, kFirstGroup = 1, kMidGroup = 2, kLastGroup = 3 };
+
 template <int D, int RT, bool MEAN, bool TAIL>
 __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, const int* lim, const Op<uint16_t, D>* yr,
-                                            const float* nlse, float* out, float s2, float log2R, int c16, int g) {
+                                            const float* nlse, float* out, float s2, float log2R, int c16, int g,
+                                            int phase, float* kacc, int k0) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
@@ -853,13 +874,24 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
         if constexpr (MEAN) {
             b += dev::shfl_xor_f(b, 16);
             b += dev::shfl_xor_f(b, 32);
-            b = (log2f(b) - log2R) * 0.69314718055994531f;  // ln of the mean weight
         } else {
             b = fmaxf(b, dev::shfl_xor_f(b, 16));
             b = fmaxf(b, dev::shfl_xor_f(b, 32));
-            b *= s2 * 0.69314718055994531f;
         }
-        if (g == t && kb + t * 16 + c16 < N) out[kb + t * 16 + c16] = b;
+        const int key = kb + t * 16 + c16;
+        if (g == t && key < N) {
+            // several row groups: the key's sum or max so far, kept by this lane
+            if (phase == kMidGroup || phase == kLastGroup) b = MEAN ? b + kacc[key - k0] : fmaxf(b, kacc[key - k0]);
+            if (phase == kFirstGroup || phase == kMidGroup) {
+                kacc[key - k0] = b;
+            } else {
+                if constexpr (MEAN)
+                    b = (log2f(b) - log2R) * 0.69314718055994531f;  // ln of the mean weight
+                else
+                    b *= s2 * 0.69314718055994531f;
+                out[key] = b;
+            }
+        }
     }
 }
 
@@ -873,9 +905,11 @@ __device__ __forceinline__ void wait_group(bool more) {
         wait_vmem<0>();
 }
 
-template <int D, int RT>
-__device__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
-                           const Op<uint16_t, D>* yr, int* s_flag) {
+// MULTI: the rows come in several row groups, each loaded here (else the
+// item's only group was loaded with its ticket).
+template <int D, int RT, bool MULTI>
+__device__ __forceinline__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
+                           Op<uint16_t, D>* yr, int* s_flag) {
     const int KC = a.key_chunk, KPW = KC / kWaves, GPW = KPW / kFKG;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -886,55 +920,68 @@ __device__ void fast_stats(const Args& a, int h, int chunk, FastSmem& sm, StageB
     const int ngroups = max(0, min(GPW, (N - kw + kFKG - 1) / kFKG));
     uint16_t* stA = sa.k[wave];
     uint16_t* stB = sb.k[wave];
-    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
-    if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+    if (!MULTI) {
+        if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
+        if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+    }
     const float s2 = a.s2;
     const KeyMask mk = key_mask(a, a.rmeta[(size_t)h * kMetaWords]);
     const int clear_below = mk.all_see_below();
-    fill_limits<RT>(mk, sm.lim);
-    __syncthreads();
-    float m[RT], z[RT];
-#pragma unroll
-    for (int i = 0; i < RT; ++i) {
-        m[i] = -INFINITY;
-        z[i] = 0.f;
-    }
-#pragma unroll 1
-    for (int kg = 0; kg < ngroups; kg += 2) {
-        const int kb = kw + kg * kFKG;
-        wait_group<D>(kg + 1 < ngroups);
-        if (kb + kFKG <= clear_below)
-            stats_group<D, RT, false>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
-        else
-            stats_group<D, RT, true>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
-        if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
-        if (kg + 1 < ngroups) {
-            wait_group<D>(kg + 2 < ngroups);
-            if (kb + 2 * kFKG <= clear_below)
-                stats_group<D, RT, false>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
-            else
-                stats_group<D, RT, true>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
-            if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
-        }
-    }
-    // lanes sharing a row: g = 0..3, then waves
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-        merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 16), dev::shfl_xor_f(z[rt], 16));
-        merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 32), dev::shfl_xor_f(z[rt], 32));
-        if (g == 0) {
-            sm.v.red.m[wave][rt * 16 + c16] = m[rt];
-            sm.v.red.z[wave][rt * 16 + c16] = z[rt];
-        }
-    }
-    __syncthreads();
     const size_t pbase = ((size_t)h * a.nch + chunk) * a.R_pad_max;
-    for (int r = tid; r < RT * 16; r += kThreads) {
-        float mm = sm.v.red.m[0][r], zz = sm.v.red.z[0][r];
+    // Rows in groups of 16 RT; the chunk's keys are streamed again for every
+    // further group.
+    const int nrg = MULTI ? a.R_pad_max / (RT * 16) : 1;
+    for (int rg = 0; rg < nrg; ++rg) {
+        if (MULTI) {
+            load_rows<D, RT>(a, h, rg, yr, lane);
+            if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
+            if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+        }
+        fill_limits<RT>(mk, rg * RT * 16, sm.lim);
+        __syncthreads();
+        float m[RT], z[RT];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) merge_mz(mm, zz, sm.v.red.m[w][r], sm.v.red.z[w][r]);
-        dev::st_coherent(a.part_m + pbase + r, mm);
-        dev::st_coherent(a.part_z + pbase + r, zz);
+        for (int i = 0; i < RT; ++i) {
+            m[i] = -INFINITY;
+            z[i] = 0.f;
+        }
+#pragma unroll 1
+        for (int kg = 0; kg < ngroups; kg += 2) {
+            const int kb = kw + kg * kFKG;
+            wait_group<D>(kg + 1 < ngroups);
+            if (kb + kFKG <= clear_below)
+                stats_group<D, RT, false>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
+            else
+                stats_group<D, RT, true>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
+            if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
+            if (kg + 1 < ngroups) {
+                wait_group<D>(kg + 2 < ngroups);
+                if (kb + 2 * kFKG <= clear_below)
+                    stats_group<D, RT, false>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
+                else
+                    stats_group<D, RT, true>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
+                if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
+            }
+        }
+        // lanes sharing a row: g = 0..3, then waves
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 16), dev::shfl_xor_f(z[rt], 16));
+            merge_mz(m[rt], z[rt], dev::shfl_xor_f(m[rt], 32), dev::shfl_xor_f(z[rt], 32));
+            if (g == 0) {
+                sm.v.red.m[wave][rt * 16 + c16] = m[rt];
+                sm.v.red.z[wave][rt * 16 + c16] = z[rt];
+            }
+        }
+        __syncthreads();
+        for (int r = tid; r < RT * 16; r += kThreads) {
+            float mm = sm.v.red.m[0][r], zz = sm.v.red.z[0][r];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) merge_mz(mm, zz, sm.v.red.m[w][r], sm.v.red.z[w][r]);
+            dev::st_coherent(a.part_m + pbase + rg * RT * 16 + r, mm);
+            dev::st_coherent(a.part_z + pbase + rg * RT * 16 + r, zz);
+        }
+        __syncthreads();  // the statistics and limits are rewritten by the next group
     }
     if (count_stats(a, h, s_flag)) {
         const int* meta = a.rmeta + (size_t)h * kMetaWords;
@@ -947,12 +994,12 @@ template <int D, int RT, bool MEAN>
 __device__ __forceinline__ void final_loop(const uint16_t* Kh, int kw, int ngroups, int N, int clear_below,
                                            const int* lim, uint16_t* stA, uint16_t* stB, const Op<uint16_t, D>* yr,
                                            const float* nlse, float* out, float s2, float log2R, int lane, int c16,
-                                           int g) {
+                                           int g, int phase, float* kacc, int k0) {
     auto body = [&](const uint16_t* st, int kb) {
         if (kb + kFKG <= clear_below)
-            final_group<D, RT, MEAN, false>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g);
+            final_group<D, RT, MEAN, false>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g, phase, kacc, k0);
         else
-            final_group<D, RT, MEAN, true>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g);
+            final_group<D, RT, MEAN, true>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g, phase, kacc, k0);
     };
 #pragma unroll 1
     for (int kg = 0; kg < ngroups; kg += 2) {
@@ -968,9 +1015,9 @@ __device__ __forceinline__ void final_loop(const uint16_t* Kh, int kw, int ngrou
     }
 }
 
-template <int D, int RT>
-__device__ void fast_final(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
-                           const Op<uint16_t, D>* yr, int* s_flag) {
+template <int D, int RT, bool MULTI>
+__device__ __forceinline__ void fast_final(const Args& a, int h, int chunk, FastSmem& sm, StageBuf<D>& sa, StageBuf<D>& sb,
+                           Op<uint16_t, D>* yr, int* s_flag) {
     const int KC = a.key_chunk, KPW = KC / kWaves, GPW = KPW / kFKG;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -990,21 +1037,32 @@ __device__ void fast_final(const Args& a, int h, int chunk, FastSmem& sm, StageB
     }
     const float inv_s2 = 1.0f / a.s2;
     const KeyMask mk = key_mask(a, a.rmeta[(size_t)h * kMetaWords]);
-    for (int r = tid; r < RT * 16; r += kThreads)
-        sm.v.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + r) * inv_s2;
-    fill_limits<RT>(mk, sm.lim);
-    __syncthreads();
     float* out = a.scores + (size_t)h * N;
     const int clear_below = mk.all_see_below();
-    if (a.mean)
-        final_loop<D, RT, true>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2,
-                                log2f((float)mk.R), lane, c16, g);
-    else
-        final_loop<D, RT, false>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2, 0.f,
-                                 lane, c16, g);
+    const float log2R = log2f((float)mk.R);
+    const int nrg = MULTI ? a.R_pad_max / (RT * 16) : 1;
+    for (int rg = 0; rg < nrg; ++rg) {
+        if (MULTI) {
+            load_rows<D, RT>(a, h, rg, yr, lane);
+            if (rg > 0 && ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
+            if (rg > 0 && ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+        }
+        for (int r = tid; r < RT * 16; r += kThreads)
+            sm.v.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + rg * RT * 16 + r) * inv_s2;
+        fill_limits<RT>(mk, rg * RT * 16, sm.lim);
+        __syncthreads();
+        const int phase = nrg == 1 ? kOnlyGroup : rg == 0 ? kFirstGroup : rg == nrg - 1 ? kLastGroup : kMidGroup;
+        if (a.mean)
+            final_loop<D, RT, true>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2,
+                                    log2R, lane, c16, g, phase, sm.kacc, chunk * KC);
+        else
+            final_loop<D, RT, false>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2,
+                                     0.f, lane, c16, g, phase, sm.kacc, chunk * KC);
+        __syncthreads();  // the normalisers and limits are rewritten by the next group
+    }
 }
 
-template <int D, int RT>
+template <int D, int RT, bool MULTI>
 __global__ __launch_bounds__(kThreads, 2) void fast_score_kernel(Args a) {
     __shared__ FastSmem sm;
     __shared__ StageBuf<D> sa;
@@ -1013,28 +1071,31 @@ __global__ __launch_bounds__(kThreads, 2) void fast_score_kernel(Args a) {
     const int h = head_of_block(a, blockIdx.x);
     const TicketReq req = request_ticket(a, h);
     Op<uint16_t, D> yr[RT];
-    load_rows<D, RT>(a, h, yr, threadIdx.x & 63);  // in flight with the ticket
+    if (!MULTI) load_rows<D, RT>(a, h, 0, yr, threadIdx.x & 63);  // in flight with the ticket
     if (!complete_ticket(a, req, &s_ticket, &s_ok)) {
         wait_vmem<0>();
         return;
     }
     const int ticket = __builtin_amdgcn_readfirstlane(s_ticket);
     if (ticket < a.nch)
-        fast_stats<D, RT>(a, h, ticket, sm, sa, sb, yr, &s_flag);
+        fast_stats<D, RT, MULTI>(a, h, ticket, sm, sa, sb, yr, &s_flag);
     else
-        fast_final<D, RT>(a, h, ticket - a.nch, sm, sa, sb, yr, &s_flag);
+        fast_final<D, RT, MULTI>(a, h, ticket - a.nch, sm, sa, sb, yr, &s_flag);
 }
 
 template <int D, int RT>
 hipError_t launch_fast_rt(const Args& a, hipStream_t s) {
     hipLaunchKernelGGL((rows_kernel<D>), dim3(a.P), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL((fast_score_kernel<D, RT>), dim3(a.total), dim3(kThreads), 0, s, a);
+    if (a.R_pad_max > RT * 16)
+        hipLaunchKernelGGL((fast_score_kernel<D, RT, true>), dim3(a.total), dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((fast_score_kernel<D, RT, false>), dim3(a.total), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
 template <int D>
-hipError_t launch_fast(const Args& a, hipStream_t s) {
-    switch (a.R_pad_max / 16) {
+hipError_t launch_fast(const Args& a, int rtg, hipStream_t s) {
+    switch (rtg) {
         case 1: return launch_fast_rt<D, 1>(a, s);
         case 2: return launch_fast_rt<D, 2>(a, s);
         case 3: return launch_fast_rt<D, 3>(a, s);
@@ -1102,10 +1163,10 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
     a.mean = (flags & BKV_SCORE_MEAN) != 0;
     a.causal = (flags & BKV_SCORE_CAUSAL) != 0;
     const bool bf = d.dtype == BKV_BF16;
-    if (bf && L.R_pad_max <= kFRT * 16) {  // all rows fit in registers
+    if (L.rtg > 0) {  // bf16: each row group's rows fit in registers
         a.rows = reinterpret_cast<uint16_t*>(w + L.rows);
         a.rmeta = reinterpret_cast<int*>(w + L.rmeta);
-        return d.D == 128 ? launch_fast<128>(a, s) : launch_fast<64>(a, s);
+        return d.D == 128 ? launch_fast<128>(a, L.rtg, s) : launch_fast<64>(a, L.rtg, s);
     }
     const bool k4 = L.kgn == 4;  // 1024-key items (else 256)
     if (bf && d.D == 128) return k4 ? launch_t<uint16_t, 128, 4>(a, s) : launch_t<uint16_t, 128, 1>(a, s);

@@ -65,3 +65,35 @@ def test_benchmark_layers_sampled_heads():
         assert_rows_match(V_gpu, ref["V"][li, hi], kg, kr, d.n_keep, "V")
         del x
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("w", [synth.QWEN25_7B_16K, synth.LLAMA8B_64K], ids=lambda w: w.name)
+def test_wide_group_layers_sampled_heads(w):
+    # the shapes whose observation rows (R = 464, 544) span several row groups
+    d = dims_of(w)
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    scores = torch.empty(d.B, d.Hkv, d.N, device="cuda")
+    kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
+    x = synth.make_layer(w, seed=200, device="cuda")
+    heads = [(0, 0), (w.B - 1, w.Hkv - 1)]
+    bsel = sorted({b for b, _ in heads})
+    xh = {k: (host(v[bsel]) if k in ("K", "V", "q_win", "beacons", "counts") else host(v)) for k, v in x.items()}
+    say(f"wide layer {w.name}: {d}")
+    bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+              rope_sin=x["rope_sin"])
+    bkv.topk(d, scores, kept)
+    bkv.compact(d, x["K"], x["V"], kept, ws)
+    torch.cuda.synchronize()
+    assert bkv.device_status(ws) == bkv.OK
+    s_all = host(scores).numpy()
+    assert not np.isnan(s_all).any() and np.all(s_all <= 1e-4)
+    hl = [(bsel.index(b), h) for b, h in heads]
+    say(f"wide layer {w.name}: oracle on {len(hl)} heads")
+    ref = oracle.evict(xh["K"], xh["V"], xh["q_win"], xh["beacons"], xh["counts"], N=w.N, budget=w.budget, W=w.W,
+                       rope_cos=xh["rope_cos"], rope_sin=xh["rope_sin"], heads=hl, threads=len(hl))
+    for (b, h), (lb, _) in zip(heads, hl):
+        assert_scores_close(s_all[b, h], ref["scores"][lb, h])
+        kg, kr = host(kept)[b, h].numpy(), ref["kept"][lb, h]
+        band, diff = compare_kept(kg[None], kr[None], ref["scores"][lb, h][None], w.N, w.W, 0, w.budget)
+        say(f"  head ({b}, {h}): tie band {band}, {diff} in-band differences")
+        assert_rows_match(host(x["K"][b, h])[None], ref["K"][lb, h][None], kg[None], kr[None], d.n_keep, "K")
