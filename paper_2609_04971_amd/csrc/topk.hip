@@ -75,6 +75,64 @@ __device__ __forceinline__ int block_excl_scan(int v, int* buf, int* total) {
     return before;
 }
 
+// Block-wide suffix scan of the kBins first-stage counts (thread t owns the
+// bins of its reversed index rt = kThreads - 1 - t, 4 rt .. 4 rt + 3, so the
+// exclusive prefix in thread order counts every higher bin): the bin at
+// which the running count from the top reaches `remaining`, and how many
+// candidates lie strictly above it.
+__device__ __forceinline__ void find_wide_digit(const int* cnt, int remaining, int* buf, int* s_digit,
+                                                int* s_above) {
+    const int rt = kThreads - 1 - (int)threadIdx.x;
+    const int d0 = 4 * rt;
+    const int c0 = cnt[d0], c1 = cnt[d0 + 1], c2 = cnt[d0 + 2], c3 = cnt[d0 + 3];
+    int total;
+    const int above = block_excl_scan(c0 + c1 + c2 + c3, buf, &total);  // bins >= 4 (rt + 1)
+    const int S3 = above + c3, S2 = S3 + c2, S1 = S2 + c1, S0 = S1 + c0;
+    const int r = remaining;
+    if (S3 >= r && above < r) { *s_digit = d0 + 3; *s_above = above; }
+    if (S2 >= r && S3 < r) { *s_digit = d0 + 2; *s_above = S3; }
+    if (S1 >= r && S2 < r) { *s_digit = d0 + 1; *s_above = S2; }
+    if (S0 >= r && S1 < r) { *s_digit = d0; *s_above = S1; }
+}
+
+// Float min / max over the block through order keys (DPP within waves, LDS
+// across them); `slot` holds kWaves words.  Every thread gets the result.
+__device__ __forceinline__ uint32_t block_min_u32(uint32_t v, uint32_t* slot) {
+    v = dev::wave_min_u32(v);
+    if ((threadIdx.x & 63) == 0) slot[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint32_t m = slot[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) m = min(m, slot[w]);
+    __syncthreads();
+    return m;
+}
+__device__ __forceinline__ float key_to_float(uint32_t k) {  // inverse of order_key (on keys it produces)
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// OR over the wave (DPP within rows, then the four rows), wave-uniform.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_or(uint32_t v) {
+    return v | (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint32_t wave_or_u32(uint32_t v) {
+    v = dpp_or<0x140>(dpp_or<0x141>(dpp_or<0x4e>(dpp_or<0xb1>(v))));
+    return (uint32_t)(__builtin_amdgcn_readlane((int)v, 0) | __builtin_amdgcn_readlane((int)v, 16) |
+                      __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
+}
+
+constexpr int kBins = 4096;    // value bins of the first stage
+constexpr int kMaxRank = 512;  // candidates ranked directly at most
+
+// Value bin of score v: monotone non-decreasing in v (each step is a
+// correctly rounded operation or a clamp), so every key in a higher bin
+// beats every key in a lower one.  -inf lands in bin 0.
+__device__ __forceinline__ int value_bin(float v, float vmin, float scale) {
+    const float t = (v - vmin) * scale;
+    return (int)fminf(fmaxf(floorf(t), 0.f), (float)(kBins - 1));
+}
+
 constexpr int kRegKeys = 32768;  // longest head whose keys stay in registers
 
 // Order keys of one head, read from global memory on every access.
@@ -87,10 +145,15 @@ struct GlobalKeys {
 template <class Keys>
 __device__ void topk_head(const float* __restrict__ scores, int32_t* __restrict__ kept, int N, int budget, int W,
                           int n_prefix, int n_keep, Keys& keys) {
-    __shared__ int hist[kWaves][256];
+    __shared__ int hist[kWaves][256];  // also the kBins value histogram
+    static_assert(kWaves * 256 == kBins, "LDS reuse");
     __shared__ int tot[256];
     __shared__ int scan_buf[kWaves + 1];
-    __shared__ int s_digit, s_above;
+    __shared__ uint32_t red[kWaves];
+    __shared__ uint32_t ck[kMaxRank];
+    __shared__ int ci[kMaxRank];
+    __shared__ int s_digit, s_above, s_ncand, s_need;
+    __shared__ uint32_t s_theta;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h = blockIdx.x;
     int32_t* out = kept + (size_t)h * n_keep;
@@ -102,10 +165,74 @@ __device__ void topk_head(const float* __restrict__ scores, int32_t* __restrict_
     keys.init(scores + (size_t)h * N, N);
     const int lo = n_prefix, hi = N - W;  // candidates [lo, hi)
     const int ksel = budget - n_prefix - W;
+    if (tid == 0) {
+        s_ncand = 0;
+        s_need = 0;
+    }
+
+    // First, as in the register kernel: value bins over [min, max] of the
+    // candidates' scores, then a direct rank of the threshold bin's keys;
+    // keys in higher bins are larger than theta, keys in lower ones smaller,
+    // so the emit below needs only theta and the number of ties to take.
+    bool decided = false;
+    uint32_t theta_v = 0;
+    int need_v = 0;
+    if (ksel > 0) {
+        constexpr uint32_t kNegInf = 0x007fffffu, kPosInf = 0xff800000u;
+        uint32_t kall = 0xffffffffu, kfin = 0xffffffffu, kmx = 0u;
+        for (int j = lo + tid; j < hi; j += kThreads) {
+            const uint32_t u = keys[j];
+            kall = min(kall, u);
+            kfin = min(kfin, u > kNegInf ? u : 0xffffffffu);
+            kmx = max(kmx, u);
+        }
+        kall = block_min_u32(kall, red);
+        kfin = block_min_u32(kfin, red);
+        kmx = ~block_min_u32(~kmx, red);
+        const float vmin = key_to_float(kfin), vmax = key_to_float(kmx);
+        const float width = vmax - vmin, scale = (float)kBins / width;
+        if (kall >= kNegInf && kmx < kPosInf && kfin < kPosInf && vmax > vmin && width < INFINITY &&
+            scale < INFINITY) {
+            int* h1 = &hist[0][0];
+            for (int i = tid; i < kBins; i += kThreads) h1[i] = 0;
+            __syncthreads();
+            for (int j = lo + tid; j < hi; j += kThreads) atomicAdd(&h1[value_bin(key_to_float(keys[j]), vmin, scale)], 1);
+            __syncthreads();
+            find_wide_digit(h1, ksel, scan_buf, &s_digit, &s_above);
+            __syncthreads();
+            const int bstar = s_digit, rem = ksel - s_above, ncand = h1[bstar];
+            if (ncand <= kMaxRank) {
+                for (int j = lo + tid; j < hi; j += kThreads) {
+                    const uint32_t u = keys[j];
+                    if (value_bin(key_to_float(u), vmin, scale) == bstar) {
+                        const int slot = atomicAdd(&s_ncand, 1);
+                        ck[slot] = u;
+                        ci[slot] = j;
+                    }
+                }
+                __syncthreads();
+                int rank = kMaxRank;
+                uint32_t mk = 0;
+                if (tid < ncand) {
+                    mk = ck[tid];
+                    const int mi = ci[tid];
+                    rank = 0;
+                    for (int c = 0; c < ncand; ++c) rank += (ck[c] > mk) || (ck[c] == mk && ci[c] < mi);
+                    if (rank == rem - 1) s_theta = mk;
+                }
+                __syncthreads();
+                if (tid < ncand && mk == s_theta && rank < rem) atomicAdd(&s_need, 1);
+                __syncthreads();
+                theta_v = s_theta;
+                need_v = s_need;
+                decided = true;
+            }
+        }
+    }
 
     uint32_t prefix = 0, pmask = 0;
     int remaining = ksel;  // how many still to take at or below the current prefix
-    if (ksel > 0) {
+    if (ksel > 0 && !decided) {
         for (int pass = 0; pass < 4; ++pass) {
             const int shift = 24 - 8 * pass;
             for (int i = tid; i < kWaves * 256; i += kThreads) (&hist[0][0])[i] = 0;
@@ -150,8 +277,9 @@ __device__ void topk_head(const float* __restrict__ scores, int32_t* __restrict_
             __syncthreads();
         }
     }
-    const uint32_t theta = prefix;
-    const int need_eq = (ksel > 0) ? remaining : 0;  // ties at theta to take, lowest index first
+    const uint32_t theta = decided ? theta_v : prefix;
+    // ties at theta to take, lowest index first
+    const int need_eq = (ksel > 0) ? (decided ? need_v : remaining) : 0;
 
     // Emit: thread t owns indices [t*per, min((t+1)*per, N)).
     const int per = (N + kThreads - 1) / kThreads;
@@ -226,26 +354,6 @@ constexpr int kPer = kRegKeys / kThreads;  // keys per thread
 constexpr int kSub = 4;                      // histogram copies per wave
 constexpr int kRows = kPer * kWaves;         // (row i, wave) runs of 64 tokens
 
-// Block-wide suffix scan of the kBins first-stage counts (thread t owns the
-// bins of its reversed index rt = kThreads - 1 - t, 4 rt .. 4 rt + 3, so the
-// exclusive prefix in thread order counts every higher bin): the bin at
-// which the running count from the top reaches `remaining`, and how many
-// candidates lie strictly above it.
-__device__ __forceinline__ void find_wide_digit(const int* cnt, int remaining, int* buf, int* s_digit,
-                                                int* s_above) {
-    const int rt = kThreads - 1 - (int)threadIdx.x;
-    const int d0 = 4 * rt;
-    const int c0 = cnt[d0], c1 = cnt[d0 + 1], c2 = cnt[d0 + 2], c3 = cnt[d0 + 3];
-    int total;
-    const int above = block_excl_scan(c0 + c1 + c2 + c3, buf, &total);  // bins >= 4 (rt + 1)
-    const int S3 = above + c3, S2 = S3 + c2, S1 = S2 + c1, S0 = S1 + c0;
-    const int r = remaining;
-    if (S3 >= r && above < r) { *s_digit = d0 + 3; *s_above = above; }
-    if (S2 >= r && S3 < r) { *s_digit = d0 + 2; *s_above = S3; }
-    if (S1 >= r && S2 < r) { *s_digit = d0 + 1; *s_above = S2; }
-    if (S0 >= r && S1 < r) { *s_digit = d0; *s_above = S1; }
-}
-
 // Add one to digit d of this lane's histogram copy.  The most common digit
 // among the wave's active lanes is counted with one atomic by its first lane
 // (digits are often concentrated, and same-address LDS atomics serialise);
@@ -275,44 +383,6 @@ __device__ __forceinline__ void scan_runs(int* c, int* buf) {
     const int before = block_excl_scan(v, buf, &total);
     if (t < kRows) c[t] = before;
     __syncthreads();
-}
-
-// Float min / max over the block through order keys (DPP within waves, LDS
-// across them); `slot` holds kWaves words.  Every thread gets the result.
-__device__ __forceinline__ uint32_t block_min_u32(uint32_t v, uint32_t* slot) {
-    v = dev::wave_min_u32(v);
-    if ((threadIdx.x & 63) == 0) slot[threadIdx.x >> 6] = v;
-    __syncthreads();
-    uint32_t m = slot[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) m = min(m, slot[w]);
-    __syncthreads();
-    return m;
-}
-__device__ __forceinline__ float key_to_float(uint32_t k) {  // inverse of order_key (on keys it produces)
-    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
-}
-
-// OR over the wave (DPP within rows, then the four rows), wave-uniform.
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_or(uint32_t v) {
-    return v | (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
-}
-__device__ __forceinline__ uint32_t wave_or_u32(uint32_t v) {
-    v = dpp_or<0x140>(dpp_or<0x141>(dpp_or<0x4e>(dpp_or<0xb1>(v))));
-    return (uint32_t)(__builtin_amdgcn_readlane((int)v, 0) | __builtin_amdgcn_readlane((int)v, 16) |
-                      __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
-}
-
-constexpr int kBins = 4096;    // value bins of the first stage
-constexpr int kMaxRank = 512;  // candidates ranked directly at most
-
-// Value bin of score v: monotone non-decreasing in v (each step is a
-// correctly rounded operation or a clamp), so every key in a higher bin
-// beats every key in a lower one.  -inf lands in bin 0.
-__device__ __forceinline__ int value_bin(float v, float vmin, float scale) {
-    const float t = (v - vmin) * scale;
-    return (int)fminf(fmaxf(floorf(t), 0.f), (float)(kBins - 1));
 }
 
 __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restrict__ scores,
