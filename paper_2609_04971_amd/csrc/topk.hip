@@ -350,9 +350,8 @@ __device__ __forceinline__ void find_digit(const int* tot, int remaining, int* s
     if (S0 >= r && S1 < r) { *s_digit = d0; *s_above = S1; }
 }
 
-constexpr int kPer = kRegKeys / kThreads;  // keys per thread
-constexpr int kSub = 4;                      // histogram copies per wave
-constexpr int kRows = kPer * kWaves;         // (row i, wave) runs of 64 tokens
+constexpr int kPerMax = kRegKeys / kThreads;  // keys per thread at most
+constexpr int kSub = 4;                         // histogram copies per wave
 
 // Add one to digit d of this lane's histogram copy.  The most common digit
 // among the wave's active lanes is counted with one atomic by its first lane
@@ -374,17 +373,20 @@ __device__ __forceinline__ int rank_in_wave(uint64_t mask) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
 }
 
-// Exclusive scan, in place, of the kRows per-run counts c[i][wave] in
+// Exclusive scan, in place, of the ROWS per-run counts c[i][wave] in
 // token order (run (i, w) covers tokens i*1024 + 64 w ... + 63).
+template <int ROWS>
 __device__ __forceinline__ void scan_runs(int* c, int* buf) {
     const int t = threadIdx.x;
-    const int v = (t < kRows) ? c[t] : 0;
+    const int v = (t < ROWS) ? c[t] : 0;
     int total;
     const int before = block_excl_scan(v, buf, &total);
-    if (t < kRows) c[t] = before;
+    if (t < ROWS) c[t] = before;
     __syncthreads();
 }
 
+// PER keys per thread (8 or 32): heads of up to 1024 PER tokens.
+template <int PER>
 __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restrict__ scores,
                                                              int32_t* __restrict__ kept, int N, int budget, int W,
                                                              int n_prefix, int n_keep) {
@@ -394,7 +396,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
     static_assert(kWaves * kSub * 256 >= kBins + 2 * kMaxRank, "LDS reuse");
     __shared__ int part[kThreads / 256][256];
     __shared__ int tot[256];
-    __shared__ int runs[kRows];
+    __shared__ int runs[PER * kWaves];
     __shared__ int scan_buf[kWaves + 1];
     __shared__ uint32_t red[kWaves];
     __shared__ uint32_t red3[3][kWaves];
@@ -413,12 +415,12 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
     const int ksel = budget - n_prefix - W;
     // key i of this thread is token tid + i * kThreads (coalesced loads, all
     // in flight at once; tokens past N read token N - 1 and are no candidates)
-    uint32_t u[kPer];
+    uint32_t u[PER];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) u[i] = order_key(srow[min(tid + i * kThreads, N - 1)]);
+    for (int i = 0; i < PER; ++i) u[i] = order_key(srow[min(tid + i * kThreads, N - 1)]);
     uint32_t pos_cand = 0;  // candidate positions (the rest are forced keeps or past N)
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
+    for (int i = 0; i < PER; ++i) {
         const int j = tid + i * kThreads;
         if (j >= lo && j < hi) pos_cand |= 1u << i;
     }
@@ -443,7 +445,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
         constexpr uint32_t kNegInf = 0x007fffffu, kPosInf = 0xff800000u;
         uint32_t kall = 0xffffffffu, kfin = 0xffffffffu, kmx = 0u;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
+        for (int i = 0; i < PER; ++i) {
             const bool c = (pos_cand >> i) & 1u;
             kall = min(kall, c ? u[i] : 0xffffffffu);
             kfin = min(kfin, (c && u[i] > kNegInf) ? u[i] : 0xffffffffu);
@@ -480,7 +482,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
             __syncthreads();
             // value bins are spread, so plain atomics rarely collide
 #pragma unroll
-            for (int i = 0; i < kPer; ++i)
+            for (int i = 0; i < PER; ++i)
                 if ((pos_cand >> i) & 1u) atomicAdd(&h1[value_bin(key_to_float(u[i]), vmin, scale)], 1);
             __syncthreads();
             find_wide_digit(h1, remaining, scan_buf, &s_digit, &s_above);
@@ -490,7 +492,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
             const int ncand = h1[bstar];
             comp = 0;
 #pragma unroll
-            for (int i = 0; i < kPer; ++i) {
+            for (int i = 0; i < PER; ++i) {
                 const int b = value_bin(key_to_float(u[i]), vmin, scale);
                 sure |= (b > bstar ? 1u : 0u) << i;
                 comp |= (b == bstar ? 1u : 0u) << i;
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
                 int* ci = h1 + kBins + kMaxRank;
                 const uint32_t wcomp = wave_or_u32(comp);  // positions where some lane competes
 #pragma unroll
-                for (int i = 0; i < kPer; ++i) {
+                for (int i = 0; i < PER; ++i) {
                     if (!((wcomp >> i) & 1u)) continue;  // wave-uniform: usually skipped
                     if ((comp >> i) & 1u) {
                         const int slot = atomicAdd(&s_ncand, 1);
@@ -543,7 +545,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
         // on v = key - (smallest competing key), over only the bits that vary
         uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i)
+        for (int i = 0; i < PER; ++i)
             if ((comp >> i) & 1u) {
                 kmin = min(kmin, u[i]);
                 kmax = max(kmax, u[i]);
@@ -553,7 +555,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
         const uint32_t key_lo = kmin;
         const int vbits = (kmax > kmin) ? 32 - __builtin_clz(kmax - kmin) : 0;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) u[i] -= key_lo;  // compared only where competing from here on
+        for (int i = 0; i < PER; ++i) u[i] -= key_lo;  // compared only where competing from here on
         uint32_t prefix = 0, pmask = 0;
         const int npass = (vbits + 7) / 8;
         for (int pass = 0; pass < npass; ++pass) {
@@ -563,7 +565,7 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
             __syncthreads();
             int* hw = &hist[wave][sub][0];
 #pragma unroll
-            for (int i = 0; i < kPer; ++i)
+            for (int i = 0; i < PER; ++i)
                 count_digit(hw, (u[i] >> shift) & 255u, ((comp >> i) & 1u) && (u[i] & pmask) == prefix);
             __syncthreads();
             {   // digit d's count: thread (d, q) sums the copies of waves 4q..4q+3
@@ -592,27 +594,27 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
     // ---- emit ------------------------------------------------------------------
     // Ties at theta are ranked in token order only when some must be left out.
     const bool rank_ties = ksel > 0 && eq_total != need_eq;
-    uint64_t eqb[kPer];
+    uint64_t eqb[PER];
     if (rank_ties) {
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
+        for (int i = 0; i < PER; ++i) {
             eqb[i] = __builtin_amdgcn_ballot_w64(((comp >> i) & 1u) && u[i] == theta);
             if (lane == 0) runs[i * kWaves + wave] = (int)__builtin_popcountll(eqb[i]);
         }
         __syncthreads();
-        scan_runs(runs, scan_buf);
+        scan_runs<PER * kWaves>(runs, scan_buf);
     }
     // forced tokens (prefix, recent window) below N, the sure candidates, and
     // the competing ones at or above theta (ties only as far as need_eq)
     uint32_t valid = 0;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) valid |= (tid + i * kThreads < N ? 1u : 0u) << i;
+    for (int i = 0; i < PER; ++i) valid |= (tid + i * kThreads < N ? 1u : 0u) << i;
     uint32_t keep = valid & ~pos_cand;
     if (ksel > 0) {
         keep |= sure;
         const uint32_t wcomp = wave_or_u32(comp);
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
+        for (int i = 0; i < PER; ++i) {
             if (!((wcomp >> i) & 1u)) continue;  // wave-uniform
             bool k = u[i] > theta;
             if (u[i] == theta) k = !rank_ties || runs[i * kWaves + wave] + rank_in_wave(eqb[i]) < need_eq;
@@ -620,16 +622,16 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
         }
     }
     if (rank_ties) __syncthreads();  // tie ranks read before the counts are reused
-    uint64_t kb[kPer];
+    uint64_t kb[PER];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
+    for (int i = 0; i < PER; ++i) {
         kb[i] = __builtin_amdgcn_ballot_w64((keep >> i) & 1u);
         if (lane == 0) runs[i * kWaves + wave] = (int)__builtin_popcountll(kb[i]);
     }
     __syncthreads();
-    scan_runs(runs, scan_buf);
+    scan_runs<PER * kWaves>(runs, scan_buf);
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
+    for (int i = 0; i < PER; ++i) {
         if ((keep >> i) & 1u) {
             const int pos = runs[i * kWaves + wave] + rank_in_wave(kb[i]);
             if (pos < n_keep) out[pos] = tid + i * kThreads;
@@ -642,8 +644,11 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
 hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hipStream_t s) {
     const int P = d.B * d.Hkv;
     const int n_keep = d.N < d.budget ? d.N : d.budget;
-    if (d.N <= kRegKeys)
-        hipLaunchKernelGGL(topk_reg_kernel, dim3(P), dim3(kThreads), 0, s, scores, kept, d.N, d.budget, d.W,
+    if (d.N <= 8 * kThreads)
+        hipLaunchKernelGGL(topk_reg_kernel<8>, dim3(P), dim3(kThreads), 0, s, scores, kept, d.N, d.budget, d.W,
+                           d.n_prefix, n_keep);
+    else if (d.N <= kRegKeys)
+        hipLaunchKernelGGL(topk_reg_kernel<kPerMax>, dim3(P), dim3(kThreads), 0, s, scores, kept, d.N, d.budget, d.W,
                            d.n_prefix, n_keep);
     else
         hipLaunchKernelGGL(topk_kernel, dim3(P), dim3(kThreads), 0, s, scores, kept, d.N, d.budget, d.W,
