@@ -60,11 +60,12 @@ WsLayout ws_layout(const bkv_dims& d) {
         L.R_pad_max = nrg * L.rtg * 16;
     }
     // key chunk per score work item: 1024 keys once there are enough chunks
-    // to fill the machine several times over, or when the rows span several
-    // row groups (each group streams the chunk again, so short chunks would
-    // spend their time on per-group set-up); else 256
+    // to fill the machine about twice (shorter items spend their time on the
+    // ticket, the rows and the epilogue: at 4K tokens and 128 heads 1024-key
+    // items score 30 % faster than 256-key ones), or when the rows span
+    // several row groups (each group streams the chunk again); else 256
     const long long big = (long long)P * ((d.N + 1023) / 1024);
-    L.kgn = (big >= 2048 || tiles > kFastTiles) ? 4 : 1;
+    L.kgn = (big >= 512 || tiles > kFastTiles) ? 4 : 1;
     L.key_chunk = 256 * L.kgn;
     L.nch = (d.N + L.key_chunk - 1) / L.key_chunk;
     L.part_m = off;
