@@ -287,6 +287,7 @@ def fps_measure(w, dev, reps=20):
         gbs = nbytes / (us * 1e-6) / 1e9
         res[name] = {"heads": H, "n": n, "m": m, "in_place": in_place, "us": round(us, 2),
                      "kernel": ("fps_gram_kernel<unsigned short, 128, 2>" if n <= 64
+                                else "fps_reg_kernel<128, 8>" if n <= 1024
                                 else "fps_stream_kernel<unsigned short, 128, 2>"),
                      "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                   "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes}}

@@ -126,6 +126,9 @@ __device__ __forceinline__ float dpp_add(float v) {
 // Sum within each quad of lanes (all four lanes hold it).
 __device__ __forceinline__ float quad_sum(float v) { return dpp_add<0x4e>(dpp_add<0xb1>(v)); }
 
+// Sum within each row of 16 lanes (every lane of the row holds it).
+__device__ __forceinline__ float row16_sum(float v) { return dpp_add<0x140>(dpp_add<0x141>(quad_sum(v))); }
+
 // Sum over the wave, the same in every lane.
 __device__ __forceinline__ float wave_sum(float v) {
     v = dpp_add<0x140>(dpp_add<0x141>(quad_sum(v)));

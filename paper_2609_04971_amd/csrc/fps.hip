@@ -3,7 +3,7 @@
 // replaces a query buffer by its selection (Section 4.2, Eq. fps_q; the
 // FPS steps of Algorithm 2).
 //
-// One head per workgroup, two kernels by set size:
+// One head per workgroup, three kernels by set size:
 //
 //  - fps_gram_kernel, n <= 64, one wave.  These are the buffers of the
 //    continual path (B_Q^max = n_beacon + n_recent rows).  The whole Gram
@@ -11,14 +11,17 @@
 //    sums; fp32 input uses the fp32 MFMA) and its diagonal gives the norms.
 //    avg_i is then a column sum, and each pick costs one LDS read per lane
 //    and a wave argmin on DPP and scalar instructions.
-//  - fps_stream_kernel, n up to 32768, 1024 threads.  Prefill-sized sets.
-//    Thread t owns rows j = t + 1024 i and keeps their S_j and 1/|q_j| in
-//    registers.  avg_i uses the regrouped sum
-//        sum_j cos(q_i, q_j) = (q_i / |q_i|) . sum_j (q_j / |q_j|),
-//    which is O(n D) instead of O(n^2 D); each pick re-reads every row once
-//    to form cos(q_j, q_r), so the kernel moves about (m + 3) n D elements.
+//  - fps_reg_kernel, bf16 and 64 < n <= 1024, 512 threads.  Prefill-sized
+//    sets held in MFMA operand registers: each pick is one MFMA pass over
+//    the head's rows against the picked row, and one barrier.
+//  - fps_stream_kernel, fp32 sets and bf16 sets past 1024 rows, n up to
+//    32768, 512 threads.  Thread t owns rows j = t + 512 i and keeps their
+//    S_j and 1/|q_j| in registers; each pick re-reads every row once to
+//    form cos(q_j, q_r), so the kernel moves about (m + 3) n D elements.
 //
-// Both take the lowest index among equal values at every argmin, treat a
+// The two larger kernels use the regrouped average
+//     sum_j cos(q_i, q_j) = (q_i / |q_i|) . sum_j (q_j / |q_j|),
+// which is O(n D) instead of O(n^2 D).  All three take the lowest index among equal values at every argmin, treat a
 // zero vector as having cosine 0 with everything, and emit the picks in
 // selection order.  The 1/n of avg_i is left out: it does not move the
 // argmin.
@@ -442,6 +445,225 @@ __global__ __launch_bounds__(kStreamThreads) void fps_stream_kernel(const T* src
     write_counts(counts, h, dst_rows, kmax, t, NT);
 }
 
+// ---- 64 < n <= 1024, bf16: rows resident in MFMA operand registers ------------
+
+constexpr int kRegThreads = 512;
+constexpr int kRegWaves = kRegThreads / 64;
+constexpr int kRegMaxNB = 8;                           // 16-row blocks per wave
+constexpr int kRegMaxN = kRegWaves * 16 * kRegMaxNB;  // 1024
+
+// Wave w holds rows 16 NB w .. 16 NB (w + 1) - 1 as NB blocks in the Gram
+// kernel's operand layout (lane (g, c16), vector v: bytes [64 v + 16 g, +16)
+// of row 16 b + c16 of the wave's block b), loaded once.  The norms, the
+// sum of unit vectors and avg_i (C21's regrouped form) come from those
+// registers.  Each pick then costs one MFMA pass per block with the picked
+// row in every column of B, so lane (g, c16) receives <q_j, q_r> for rows
+// 16 b + 4 g + v, where it keeps their S_j and 1/|q_j|.  Every wave posts
+// its best (S, j) key and the candidate row itself (operand order) to LDS,
+// so a single barrier per pick settles the argmin and hands every wave the
+// picked row.  Nothing is re-read from memory until the gather.
+template <int D, int NB>
+__global__ __launch_bounds__(kRegThreads) void fps_reg_kernel(const uint16_t* src, int src_rows, int n, int kmax,
+                                                             int32_t* picks, void* dst, int widen, int dst_rows,
+                                                             int32_t* counts) {
+    constexpr int NV = Blk<uint16_t, D>::NV;
+    constexpr int RW = 16 * NB;  // rows per wave
+    constexpr int CPR = D * 2 / 16;
+    __shared__ __attribute__((aligned(16))) float rinv_s[kRegWaves * RW];  // 1/|q_j| of every row
+    __shared__ __attribute__((aligned(16))) float rs0_s[kRegWaves * RW];   // avg_j times n
+    __shared__ __attribute__((aligned(16))) float part[kRegWaves][D];      // per-wave sums of unit vectors
+    __shared__ __attribute__((aligned(16))) float uvec[D];
+    __shared__ u32x4 cand[2][kRegWaves][NV * 4];                            // each wave's candidate row
+    __shared__ unsigned long long wkey[2][kRegWaves];
+    __shared__ int spick[kMaxGather];
+    const int t = threadIdx.x, lane = t & 63, g = lane >> 4, c16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int h = blockIdx.x;
+    const uint16_t* qh = src + (size_t)h * src_rows * D;
+    const int row0 = w * RW;
+
+    Blk<uint16_t, D> q[NB];
+    dev::static_for<NB>([&](auto b) { load_blk<uint16_t, D>(q[b], qh, row0 + 16 * b, n, lane); });
+
+    // norms (rows past n are zero: inverse norm 0) and the wave's sum of
+    // unit vectors, lane (g, c16) adding elements 32 v + 8 g + e of its rows
+    float usum[NV][8];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) usum[v][e] = 0.f;
+    dev::static_for<NB>([&](auto b) {
+        float p = 0.f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            float f[8];
+            Elt<uint16_t>::unpack(q[b].v[v], f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) p = fmaf(f[e], f[e], p);
+        }
+        p += dev::shfl_xor_f(p, 16);
+        p += dev::shfl_xor_f(p, 32);
+        const float inv = inv_norm(p);
+        if (g == 0) rinv_s[row0 + 16 * b + c16] = inv;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            float f[8];
+            Elt<uint16_t>::unpack(q[b].v[v], f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) usum[v][e] = fmaf(f[e], inv, usum[v][e]);
+        }
+    });
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float s = dev::row16_sum(usum[v][e]);  // over the 16 lanes of group g
+            if (c16 == 0) part[w][32 * v + 8 * g + e] = s;
+        }
+    __syncthreads();
+    if (t < D) {
+        float s = 0.f;
+#pragma unroll
+        for (int x = 0; x < kRegWaves; ++x) s += part[x][t];
+        uvec[t] = s;
+    }
+    __syncthreads();
+    // avg_j times n = (q_j . sum of unit vectors) / |q_j|
+    dev::static_for<NB>([&](auto b) {
+        float p = 0.f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            float f[8];
+            Elt<uint16_t>::unpack(q[b].v[v], f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) p = fmaf(f[e], uvec[32 * v + 8 * g + e], p);
+        }
+        p += dev::shfl_xor_f(p, 16);
+        p += dev::shfl_xor_f(p, 32);
+        if (g == 0) rs0_s[row0 + 16 * b + c16] = p * rinv_s[row0 + 16 * b + c16];
+    });
+    __syncthreads();
+    // The 16 lanes of lane group g all receive the MFMA results for rows
+    // 16 b + 4 g + v (b < NB, v < 4); lane c16 tracks CPL of them, number
+    // cg = CPL c16 + c: block cg / 4, v = cg % 4.  Its S_j and 1/|q_j| stay
+    // in registers.
+    constexpr int CPL = NB >= 4 ? NB / 4 : 1;
+    float S[CPL], cinv[CPL];
+    unsigned done = 0;  // bit c: candidate c picked, past n, or absent
+    auto cand_row = [&](int c) {
+        const int cg = c16 * CPL + c;
+        return row0 + 16 * (cg >> 2) + 4 * g + (cg & 3);
+    };
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+        const int row = cand_row(c);
+        const bool live = c16 * CPL + c < 4 * NB && row < n;
+        S[c] = live ? rs0_s[row] : 0.f;
+        cinv[c] = live ? rinv_s[row] : 0.f;
+        if (!live) done |= 1u << c;
+    }
+
+    for (int k = 0; k < kmax; ++k) {
+        const int buf = k & 1;
+        // (S, j) lexicographic minimum over the wave's unpicked rows
+        unsigned long long best = ~0ull;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const unsigned long long key = ((unsigned long long)dev::ord_key(S[c]) << 32) | (unsigned)cand_row(c);
+            if (!((done >> c) & 1u) && key < best) best = key;
+        }
+        const unsigned long long wb = dev::wave_min_u64(best);
+        const unsigned wlo = __builtin_amdgcn_readfirstlane((unsigned)wb);
+        const unsigned whi = __builtin_amdgcn_readfirstlane((unsigned)(wb >> 32));
+        if (whi != ~0u || wlo != ~0u) {
+            // the wave's candidate row, from the operand registers of the
+            // four lanes that hold it
+            const int jl = (int)wlo - row0, bb = jl >> 4;
+            if (c16 == (jl & 15)) {
+                dev::static_for<NB>([&](auto b) {
+                    if (b == bb) {
+#pragma unroll
+                        for (int v = 0; v < NV; ++v) cand[buf][w][4 * v + g] = q[b].v[v];
+                    }
+                });
+            }
+        }
+        if (lane == 0) wkey[buf][w] = ((unsigned long long)whi << 32) | wlo;
+        __syncthreads();
+        // the double-buffered posts let the next pick write without a second
+        // barrier: every wave has read these before it passes the next one
+        unsigned long long gb = ~0ull;
+        int ws = 0;
+#pragma unroll
+        for (int x = 0; x < kRegWaves; ++x) {
+            const unsigned long long y = wkey[buf][x];
+            if (y < gb) {
+                gb = y;
+                ws = x;
+            }
+        }
+        // an unpicked row exists while k < min(m, n); the clamp only keeps
+        // the reads below in bounds whatever the keys hold
+        const int r = min(max(__builtin_amdgcn_readfirstlane((int)(unsigned)gb), 0), n - 1);
+        ws = __builtin_amdgcn_readfirstlane(ws);
+        const float rinv = rinv_s[r];
+        Blk<uint16_t, D> pr;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) pr.v[v] = cand[buf][ws][4 * v + g];
+        if (t == 0) {
+            if (picks) picks[(size_t)h * kmax + k] = r;
+            if (k < kMaxGather) spick[k] = r;
+        }
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+            if (cand_row(c) == r) done |= 1u << c;
+        // <q_j, q_r> for every row of the wave; each lane keeps its own
+        float dot[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) dot[c] = 0.f;
+        dev::static_for<NB>([&](auto b) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            gram_mma<D>(acc, q[b], pr);
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                const int cg = c16 * CPL + c;
+                if ((cg >> 2) == b) {
+                    const int v = cg & 3;
+                    dot[c] = v == 0 ? acc[0] : v == 1 ? acc[1] : v == 2 ? acc[2] : acc[3];
+                }
+            }
+        });
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const float cs = dot[c] * cinv[c] * rinv;
+            S[c] = (k == 0) ? cs : fmaxf(S[c], cs);
+        }
+    }
+    __syncthreads();  // spick complete
+
+    if (dst) {
+        // every chunk of every picked row is in registers on every wave
+        // before any wave stores, so dst may be src
+        constexpr int IT = (kMaxGather * CPR + kRegThreads - 1) / kRegThreads;
+        u32x4 bufr[IT];
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            const int c = t + kRegThreads * it, i = c / CPR, piece = c % CPR;
+            bufr[it] = (i < kmax) ? load16(qh + (size_t)spick[i] * D + piece * 8) : u32x4{0u, 0u, 0u, 0u};
+        }
+        dev::wait_all_memory();
+        __syncthreads();
+        const size_t drow_bytes = (size_t)D * (widen ? 4 : 2);
+        char* dh = static_cast<char*>(dst) + (size_t)h * dst_rows * drow_bytes;
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+            const int c = t + kRegThreads * it, i = c / CPR, piece = c % CPR;
+            if (i < kmax) store_chunk<uint16_t, D>(dh + (size_t)i * drow_bytes, piece, bufr[it], widen);
+        }
+    }
+    write_counts(counts, h, dst_rows, kmax, t, kRegThreads);
+}
+
 template <typename T, int D>
 hipError_t launch_typed(int H, int n, int kmax, const void* src, int src_rows, int32_t* picks, void* dst, int widen,
                         int dst_rows, int32_t* counts, hipStream_t s) {
@@ -454,6 +676,19 @@ hipError_t launch_typed(int H, int n, int kmax, const void* src, int src_rows, i
             case 3: hipLaunchKernelGGL((fps_gram_kernel<T, D, 3>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts); break;
             default: hipLaunchKernelGGL((fps_gram_kernel<T, D, 4>), grid, block, 0, s, q, src_rows, n, kmax, picks, dst, widen, dst_rows, counts); break;
         }
+        return hipGetLastError();
+    }
+    if (sizeof(T) == 2 && n <= kRegMaxN) {
+        const uint16_t* qb = reinterpret_cast<const uint16_t*>(src);
+        const dim3 grid(H), block(kRegThreads);
+#define BKV_FPS_REG(NB) \
+    hipLaunchKernelGGL((fps_reg_kernel<D, NB>), grid, block, 0, s, qb, src_rows, n, kmax, picks, dst, widen, dst_rows, counts)
+        const int nb = (n + 16 * kRegWaves - 1) / (16 * kRegWaves);
+        if (nb <= 1) BKV_FPS_REG(1);
+        else if (nb <= 2) BKV_FPS_REG(2);
+        else if (nb <= 4) BKV_FPS_REG(4);
+        else BKV_FPS_REG(kRegMaxNB);
+#undef BKV_FPS_REG
         return hipGetLastError();
     }
     const int rows_per_thread = (n + kStreamThreads - 1) / kStreamThreads;

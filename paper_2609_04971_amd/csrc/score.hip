@@ -882,15 +882,15 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
         if (g == t && key < N) {
             // several row groups: the key's sum or max so far, kept by this lane
             if (phase == kMidGroup || phase == kLastGroup) b = MEAN ? b + kacc[key - k0] : fmaxf(b, kacc[key - k0]);
-            if (phase == kFirstGroup || phase == kMidGroup) {
-                kacc[key - k0] = b;
-            } else {
+            if (phase == kOnlyGroup || phase == kLastGroup) {
                 if constexpr (MEAN)
                     b = (log2f(b) - log2R) * 0.69314718055994531f;  // ln of the mean weight
                 else
                     b *= s2 * 0.69314718055994531f;
-                out[key] = b;
             }
+            // the item's scores are stored after its key loop: a store here
+            // would count in vmcnt, and the next group's wait would wait for it
+            kacc[key - k0] = b;
         }
     }
 }
@@ -1060,6 +1060,9 @@ __device__ __forceinline__ void fast_final(const Args& a, int h, int chunk, Fast
                                      0.f, lane, c16, g, phase, sm.kacc, chunk * KC);
         __syncthreads();  // the normalisers and limits are rewritten by the next group
     }
+    // the item's scores, kept in LDS by the key loop, go out coalesced
+    const int k0 = chunk * KC, nk = min(KC, N - k0);
+    for (int i = tid; i < nk; i += kThreads) out[k0 + i] = sm.kacc[i];
 }
 
 template <int D, int RT, bool MULTI>

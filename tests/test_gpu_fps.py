@@ -108,12 +108,13 @@ def test_fps_hand_worked_example(dtype):
     assert host(picks)[0].tolist() == [int(v) for v in fx["tie_picks"][0]]
 
 
-@pytest.mark.parametrize("reps", [1, 17, 300, 8192])
+@pytest.mark.parametrize("reps", [1, 17, 64, 256, 300, 8192])
 def test_fps_repeated_axes_closed_form(reps):
     # rows 4i..4i+3 = e0, e1, -e0, -e1: every average cosine is exactly 0,
     # so the picks are 0 (lowest index), 2 (cos -1), 1 and 3 (S = 0, lowest
     # first), then the remaining rows in index order (all at S = 1).  This
-    # runs both kernels, up to n = 32768 (64 rows per thread).
+    # runs every kernel: the Gram kernel (n <= 64), the register-resident
+    # one (bf16, n <= 1024) and the streaming one, up to n = 32768.
     q, _ = _golden("tie_query", 128)
     n = 4 * reps
     x = torch.from_numpy(np.tile(q[0], (reps, 1))[None]).to(torch.bfloat16).cuda()
@@ -137,8 +138,12 @@ def test_fps_small_sets(dtype, D, n, m, H):
     say(f"fps {dtype} D={D} n={n} m={m} H={H}: {ex}/{tot} picks exact before the first near tie")
 
 
+# bf16 sets of 65 to 1024 rows run the register-resident kernel (16-row
+# blocks, 1, 2, 4 or 8 per wave); fp32 sets and larger ones stream.
 STREAM_CASES = [("bf16", 128, 65, 16, 6), ("bf16", 128, 200, 100, 3), ("fp32", 64, 1000, 16, 3),
-                ("bf16", 128, 2500, 32, 2), ("bf16", 64, 4600, 16, 1)]
+                ("bf16", 128, 2500, 32, 2), ("bf16", 64, 4600, 16, 1), ("bf16", 128, 1024, 16, 4),
+                ("bf16", 64, 777, 40, 3), ("bf16", 128, 513, 64, 2), ("bf16", 128, 129, 129, 2),
+                ("bf16", 64, 400, 16, 3), ("fp32", 128, 1024, 16, 2)]
 
 
 @pytest.mark.parametrize("dtype,D,n,m,H", STREAM_CASES)
@@ -158,7 +163,7 @@ def test_fps_largest_sets_greedy_rule(n):
     check_greedy_rule(host(q), host(picks), 16)
 
 
-@pytest.mark.parametrize("n", [40, 300])
+@pytest.mark.parametrize("n", [40, 300, 1000])
 def test_fps_zero_and_duplicate_rows(n):
     q = queries(4, n, 128, "bf16", seed=5)
     g = torch.Generator(device="cpu").manual_seed(n)
@@ -199,7 +204,7 @@ def test_fps_empty_calls_leave_outputs():
 
 # ---- gather -------------------------------------------------------------------------
 @pytest.mark.parametrize("n,m,D,dtype", [(32, 16, 128, "bf16"), (64, 64, 64, "fp32"), (300, 128, 128, "bf16"),
-                                         (1000, 100, 64, "fp32")])
+                                         (1000, 100, 64, "fp32"), (1024, 128, 128, "bf16"), (700, 33, 64, "bf16")])
 def test_fps_gather_in_place(n, m, D, dtype):
     q = queries(24, n, D, dtype, seed=n + m)
     orig = host(q).clone()
