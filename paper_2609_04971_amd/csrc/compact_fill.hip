@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kCopyThreads) void fill_copy_kernel(char* K, char* 
         const int which = e / (kCopyRows * VPR);
         const int r = (e / VPR) % kCopyRows, v = e % VPR;
         if (r < rows && s_src[r] != j0 + r)
-            buf[k] = reinterpret_cast<const dev::u32x4*>((which ? Vh : Kh) + (size_t)s_src[r] * RB)[v];
+            buf[k] = __builtin_nontemporal_load(reinterpret_cast<const dev::u32x4*>((which ? Vh : Kh) + (size_t)s_src[r] * RB) + v);
     });
     dev::static_for<NV>([&](auto kc) {
         constexpr int k = decltype(kc)::value;
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kCopyThreads) void fill_copy_kernel(char* K, char* 
         const int which = e / (kCopyRows * VPR);
         const int r = (e / VPR) % kCopyRows, v = e % VPR;
         if (r < rows && s_src[r] != j0 + r)
-            reinterpret_cast<dev::u32x4*>((which ? Vh : Kh) + (size_t)(j0 + r) * RB)[v] = buf[k];
+            __builtin_nontemporal_store(buf[k], reinterpret_cast<dev::u32x4*>((which ? Vh : Kh) + (size_t)(j0 + r) * RB) + v);
     });
 }
 

@@ -707,8 +707,10 @@ __device__ __forceinline__ int group_offset(int j, int lane) {
 
 // Start loading keys [kb, kb + 32) of the head into a wave's stage.  The
 // buffer resource covers keys [kb, min(N, kb + 32)) only, so rows past N
-// read as zero.
-template <int D>
+// read as zero.  AUX is the load's cache policy: F items, the last readers
+// of their keys, load them non-temporal (2), which measured about 2 %
+// faster on the 32K layer than the default policy.
+template <int D, int AUX = 0>
 __device__ __forceinline__ void issue_group(const uint16_t* Kh, int kb, int N, uint16_t* stage, int lane) {
 #if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist in device code only
     using KS = KeyStage<D>;
@@ -721,7 +723,7 @@ __device__ __forceinline__ void issue_group(const uint16_t* Kh, int kb, int N, u
 #pragma unroll
     for (int j = 0; j < KS::NI; ++j)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + j * 512),
-                                                 16, group_offset<D>(j, l), 0, 0, 0);
+                                                 16, group_offset<D>(j, l), 0, 0, AUX);
 #endif
 }
 
@@ -1006,11 +1008,11 @@ __device__ __forceinline__ void final_loop(const uint16_t* Kh, int kw, int ngrou
         const int kb = kw + kg * kFKG;
         wait_group<D>(kg + 1 < ngroups);
         body(stA, kb);
-        if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
+        if (kg + 2 < ngroups) issue_group<D, 2>(Kh, kb + 2 * kFKG, N, stA, lane);
         if (kg + 1 < ngroups) {
             wait_group<D>(kg + 2 < ngroups);
             body(stB, kb + kFKG);
-            if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
+            if (kg + 3 < ngroups) issue_group<D, 2>(Kh, kb + 3 * kFKG, N, stB, lane);
         }
     }
 }
@@ -1029,8 +1031,8 @@ __device__ __forceinline__ void fast_final(const Args& a, int h, int chunk, Fast
     uint16_t* stA = sa.k[wave];
     uint16_t* stB = sb.k[wave];
     // both stages in flight while lse is awaited
-    if (ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
-    if (ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+    if (ngroups > 0) issue_group<D, 2>(Kh, kw, N, stA, lane);
+    if (ngroups > 1) issue_group<D, 2>(Kh, kw + kFKG, N, stB, lane);
     if (!await_lse(a, h, s_flag)) {
         wait_vmem<0>();  // no load may land in LDS after this workgroup ends
         return;
@@ -1044,8 +1046,8 @@ __device__ __forceinline__ void fast_final(const Args& a, int h, int chunk, Fast
     for (int rg = 0; rg < nrg; ++rg) {
         if (MULTI) {
             load_rows<D, RT>(a, h, rg, yr, lane);
-            if (rg > 0 && ngroups > 0) issue_group<D>(Kh, kw, N, stA, lane);
-            if (rg > 0 && ngroups > 1) issue_group<D>(Kh, kw + kFKG, N, stB, lane);
+            if (rg > 0 && ngroups > 0) issue_group<D, 2>(Kh, kw, N, stA, lane);
+            if (rg > 0 && ngroups > 1) issue_group<D, 2>(Kh, kw + kFKG, N, stB, lane);
         }
         for (int r = tid; r < RT * 16; r += kThreads)
             sm.v.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + rg * RT * 16 + r) * inv_s2;
