@@ -221,11 +221,13 @@ def test_fps_gather_in_place(n, m, D, dtype):
     assert torch.equal(after[:, :, k:], orig[:, :, k:])
 
 
-def test_fps_gather_into_beacon_layout_feeds_scoring():
+@pytest.mark.parametrize("n", [32, 150, 600])
+def test_fps_gather_into_beacon_layout_feeds_scoring(n):
     # per-query-head FPS of a bf16 buffer [B, Hq, n, D], widened to fp32 into
     # [B, Hq, n_beacon, D] == [B, Hkv, G * n_beacon, D]: the group-level union
-    # of beacon sets, with counts marking every slot occupied
-    B, Hq, Hkv, D, n, nb = 2, 8, 2, 128, 32, 16
+    # of beacon sets, with counts marking every slot occupied (n = 32 runs
+    # the Gram kernel, 150 and 600 the register-resident one)
+    B, Hq, Hkv, D, nb = 2, 8, 2, 128, 16
     G = Hq // Hkv
     buf = queries(Hq, n, D, "bf16", seed=3, B=B)
     beacons = torch.full((B, Hkv, G * nb, D), 5.0, device="cuda")
@@ -288,11 +290,12 @@ def test_fps_continual_compress_full_size():
     say(f"continual compress: {ex}/{tot} sampled picks exact before the first near tie")
 
 
-def test_fps_prefill_initialisation_full_size():
-    # prefill: FPS over a 4096-token prompt's pre-RoPE queries per query head
+@pytest.mark.parametrize("T", [1024, 4096])
+def test_fps_prefill_initialisation_full_size(T):
+    # prefill: FPS over a T-token prompt's pre-RoPE queries per query head
     # (B=16, Hq=32), the selection written into the heads' 32-row buffers
+    # (1024 rows run the register-resident kernel, 4096 the streaming one)
     w = synth.QWEN3_4B_32K
-    T = 4096
     q = queries(w.Hq, T, w.D, "bf16", seed=2, B=16)
     obs = torch.zeros(16, w.Hq, 32, w.D, dtype=torch.bfloat16, device="cuda")
     picks = torch.empty(16, w.Hq, 16, dtype=torch.int32, device="cuda")
