@@ -73,7 +73,9 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Args a) {
         const int src = kh[i0 + tid];
         s_src[tid] = src;
         if (src != i0 + tid) s_move = 1;  // benign race: any writer stores 1
-        if (src < i0 + tid || src >= a.N) s_bad = 1;  // not an ascending index into [0, N)
+        // not a strictly ascending index into [0, N): the hazard waits below
+        // rely on every segment's sources lying in [first, last] of its own
+        if (src < i0 + tid || src >= a.N || (i0 + tid > 0 && src <= kh[i0 + tid - 1])) s_bad = 1;
     }
     __syncthreads();
     if (s_bad && tid == 0) dev::raise_error(a.hdr, kErrBadIndex);

@@ -172,6 +172,17 @@ __device__ __forceinline__ void merge_mz(float& m, float& z, float m2, float z2)
     m = M;
 }
 
+// Mean form: fold four log2 weights y (one key, four rows) into the key's
+// running (max m, sum z of exp2(y - m)), so that no weight underflows the
+// fp32 range however small all of them are; z >= 1 once m is finite.
+__device__ __forceinline__ void add_weights(float& m, float& z, f32x4 y) {
+    const float mnew = fmaxf(m, fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])));
+    const float ms = (mnew == -INFINITY) ? 0.f : mnew;  // no row sees the key yet: z stays 0
+    z = z * fast_exp2(m - ms) + ((fast_exp2(y[0] - ms) + fast_exp2(y[1] - ms)) +
+                                 (fast_exp2(y[2] - ms) + fast_exp2(y[3] - ms)));
+    m = mnew;
+}
+
 template <typename T>
 __device__ __forceinline__ T to_elem(float f);
 template <>
@@ -204,7 +215,8 @@ struct alignas(16) Smem {
     float red_m[kWaves][Tr<T>::RG];
     float red_z[kWaves][Tr<T>::RG];
     float nlse[Tr<T>::RG];
-    float best[kWaves * 64 * 4];  // F items: per-key maxima of the chunk (up to 1024 keys)
+    float best[kWaves * 64 * 4];   // F items: per-key maxima of the chunk (up to 1024 keys)
+    float bests[kWaves * 64 * 4];  // F items, mean form: per-key weight sums relative to best
     int act[kMaxC];
     int nact;
 };
@@ -437,7 +449,10 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     const float inv_s2 = 1.0f / a.s2, s2 = a.s2;
     const KeyMask mk = key_mask(a, sm.nact);
     const bool mean = a.mean != 0;
-    for (int i = tid; i < KC; i += kThreads) sm.best[i] = mean ? 0.f : -INFINITY;
+    for (int i = tid; i < KC; i += kThreads) {
+        sm.best[i] = -INFINITY;
+        sm.bests[i] = 0.f;
+    }
     const int ngroups = max(0, min(KGN, (N - kw + 63) / 64));
 
     for (int r0 = 0; r0 < Rp; r0 += RG) {
@@ -453,9 +468,14 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
             Op<T, D> kop[4];
             load_group<T, D>(kop, Kh, kb, N, c16, g);
             const bool masked = kb + 64 > mk.all_see_below();
-            float best[4];
+            // per key of this lane: the max over rows of acc * s2 (log2 of the
+            // weight) and, for the mean, the sum of the weights relative to it
+            float best[4], bsum[4];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) best[t] = mean ? 0.f : -INFINITY;
+            for (int t = 0; t < 4; ++t) {
+                best[t] = -INFINITY;
+                bsum[t] = 0.f;
+            }
 #pragma unroll
             for (int rt = 0; rt < RTM; ++rt) {
                 if (rt < RT) {
@@ -473,8 +493,7 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
                         }
                         mma(acc, yop, kop[t]);  // rows = observation rows, columns = keys
                         if (mean)
-                            best[t] += (fast_exp2(acc[0] * s2) + fast_exp2(acc[1] * s2)) +
-                                       (fast_exp2(acc[2] * s2) + fast_exp2(acc[3] * s2));
+                            add_weights(best[t], bsum[t], acc * s2);
                         else
                             best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
                     }
@@ -485,9 +504,10 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
                 float b = best[t];
                 float* slot = sm.best + (kb - k0) + t * 16 + c16;  // this wave's own keys
                 if (mean) {
-                    b += dev::shfl_xor_f(b, 16);
-                    b += dev::shfl_xor_f(b, 32);
-                    if (g == t) *slot += b;
+                    float bs = bsum[t];
+                    merge_mz(b, bs, dev::shfl_xor_f(b, 16), dev::shfl_xor_f(bs, 16));
+                    merge_mz(b, bs, dev::shfl_xor_f(b, 32), dev::shfl_xor_f(bs, 32));
+                    if (g == t) merge_mz(*slot, sm.bests[slot - sm.best], b, bs);
                 } else {
                     b = fmaxf(b, dev::shfl_xor_f(b, 16));
                     b = fmaxf(b, dev::shfl_xor_f(b, 32));
@@ -501,7 +521,8 @@ __device__ void final_item(const Args& a, int h, int chunk, Smem<T, D>& sm, int*
     const float log2R = log2f((float)R);
     for (int i = tid; i < KC; i += kThreads)
         if (k0 + i < N)
-            out[k0 + i] = mean ? (log2f(sm.best[i]) - log2R) * 0.69314718055994531f : sm.best[i] * a.s2ln2;
+            out[k0 + i] = mean ? (sm.best[i] + log2f(sm.bests[i]) - log2R) * 0.69314718055994531f
+                               : sm.best[i] * a.s2ln2;
 }
 
 // Workgroup -> head.  The grid lists, for s = 0, 1, ..., nch workgroups of
@@ -630,11 +651,14 @@ struct alignas(16) FastSmem {
         struct {
             float m[kWaves][kFRT * 16];
             float z[kWaves][kFRT * 16];
-        } red;                  // S items: per-wave row statistics
-        float nlse[kFRT * 16];  // F items: -lse of each row (raw-dot units)
+        } red;  // S items: per-wave row statistics
+        struct {
+            float nlse[kFRT * 16];      // -lse of each row (raw-dot units)
+            float kacc[kMaxKeyChunk];   // each key's result (with several row groups: so far)
+            float kaccs[kMaxKeyChunk];  // mean form, several row groups: each key's weight sum so far
+        } fin;  // F items
     } v;
-    int lim[kFRT * 16];         // last key each row sees (KeyMask::limit)
-    float kacc[kMaxKeyChunk];   // F items with several row groups: each key's result so far
+    int lim[kFRT * 16];  // last key each row sees (KeyMask::limit)
 };
 
 // Each row's key limit into LDS (rows r0 .. r0 + 16 RT - 1), for the groups
@@ -803,13 +827,14 @@ enum RowPhase : int { kOnlyGroup = 0, kFirstGroup = 1, kMidGroup = 2, kLastGroup
 template <int D, int RT, bool MEAN, bool TAIL>
 __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, const int* lim, const Op<uint16_t, D>* yr,
                                             const float* nlse, float* out, float s2, float log2R, int c16, int g,
-                                            int phase, float* kacc, int k0) {
+                                            int phase, float* kacc, float* kaccs, int k0) {
     Op<uint16_t, D> kop[2];
     read_key_tile<D>(kop[0], st, 0, c16, g);
     read_key_tile<D>(kop[1], st, 1, c16, g);
-    // per key of this lane: max of (l - lse) / s2 over rows, or the sum of
-    // the weights exp2(s2 * acc) for the mean
-    float best[2] = {MEAN ? 0.f : -INFINITY, MEAN ? 0.f : -INFINITY};
+    // per key of this lane: max over rows of (l - lse) / s2; for the mean,
+    // the max of the log2 weights s2 * acc and the weights' sum relative to it
+    float best[2] = {-INFINITY, -INFINITY};
+    float bsum[2] = {0.f, 0.f};
     f32x4 acc[2][2];
     f32x4 cn[2];
     auto load_c = [&](int rt) {
@@ -821,8 +846,7 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             if constexpr (MEAN)
-                best[t] += (fast_exp2(a[t][0] * s2) + fast_exp2(a[t][1] * s2)) +
-                           (fast_exp2(a[t][2] * s2) + fast_exp2(a[t][3] * s2));
+                add_weights(best[t], bsum[t], a[t] * s2);
             else
                 best[t] = fmaxf(best[t], fmaxf(fmaxf(a[t][0], a[t][1]), fmaxf(a[t][2], a[t][3])));
         }
@@ -865,30 +889,37 @@ __device__ __forceinline__ void final_group(const uint16_t* st, int kb, int N, c
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, MEAN ? 4 : 1, 0);  // VALU
+            __builtin_amdgcn_sched_group_barrier(0x002, MEAN ? 6 : 1, 0);  // VALU
         }
         __builtin_amdgcn_sched_barrier(0);
     });
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-        float b = best[t];
+        float b = best[t], bs = bsum[t];
         if constexpr (MEAN) {
-            b += dev::shfl_xor_f(b, 16);
-            b += dev::shfl_xor_f(b, 32);
+            merge_mz(b, bs, dev::shfl_xor_f(b, 16), dev::shfl_xor_f(bs, 16));
+            merge_mz(b, bs, dev::shfl_xor_f(b, 32), dev::shfl_xor_f(bs, 32));
         } else {
             b = fmaxf(b, dev::shfl_xor_f(b, 16));
             b = fmaxf(b, dev::shfl_xor_f(b, 32));
         }
         const int key = kb + t * 16 + c16;
         if (g == t && key < N) {
-            // several row groups: the key's sum or max so far, kept by this lane
-            if (phase == kMidGroup || phase == kLastGroup) b = MEAN ? b + kacc[key - k0] : fmaxf(b, kacc[key - k0]);
+            // several row groups: the key's (max, sum) or max so far, kept by this lane
+            if (phase == kMidGroup || phase == kLastGroup) {
+                if constexpr (MEAN)
+                    merge_mz(b, bs, kacc[key - k0], kaccs[key - k0]);
+                else
+                    b = fmaxf(b, kacc[key - k0]);
+            }
             if (phase == kOnlyGroup || phase == kLastGroup) {
                 if constexpr (MEAN)
-                    b = (log2f(b) - log2R) * 0.69314718055994531f;  // ln of the mean weight
+                    b = (b + log2f(bs) - log2R) * 0.69314718055994531f;  // ln of the mean weight
                 else
                     b *= s2 * 0.69314718055994531f;
+            } else if constexpr (MEAN) {
+                kaccs[key - k0] = bs;
             }
             // the item's scores are stored after its key loop: a store here
             // would count in vmcnt, and the next group's wait would wait for it
@@ -996,12 +1027,14 @@ template <int D, int RT, bool MEAN>
 __device__ __forceinline__ void final_loop(const uint16_t* Kh, int kw, int ngroups, int N, int clear_below,
                                            const int* lim, uint16_t* stA, uint16_t* stB, const Op<uint16_t, D>* yr,
                                            const float* nlse, float* out, float s2, float log2R, int lane, int c16,
-                                           int g, int phase, float* kacc, int k0) {
+                                           int g, int phase, float* kacc, float* kaccs, int k0) {
     auto body = [&](const uint16_t* st, int kb) {
         if (kb + kFKG <= clear_below)
-            final_group<D, RT, MEAN, false>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g, phase, kacc, k0);
+            final_group<D, RT, MEAN, false>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g, phase, kacc, kaccs,
+                                            k0);
         else
-            final_group<D, RT, MEAN, true>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g, phase, kacc, k0);
+            final_group<D, RT, MEAN, true>(st, kb, N, lim, yr, nlse, out, s2, log2R, c16, g, phase, kacc, kaccs,
+                                           k0);
     };
 #pragma unroll 1
     for (int kg = 0; kg < ngroups; kg += 2) {
@@ -1050,21 +1083,21 @@ __device__ __forceinline__ void fast_final(const Args& a, int h, int chunk, Fast
             if (rg > 0 && ngroups > 1) issue_group<D, 2>(Kh, kw + kFKG, N, stB, lane);
         }
         for (int r = tid; r < RT * 16; r += kThreads)
-            sm.v.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + rg * RT * 16 + r) * inv_s2;
+            sm.v.fin.nlse[r] = -dev::ld_coherent(a.lse2 + (size_t)h * a.R_pad_max + rg * RT * 16 + r) * inv_s2;
         fill_limits<RT>(mk, rg * RT * 16, sm.lim);
         __syncthreads();
         const int phase = nrg == 1 ? kOnlyGroup : rg == 0 ? kFirstGroup : rg == nrg - 1 ? kLastGroup : kMidGroup;
         if (a.mean)
-            final_loop<D, RT, true>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2,
-                                    log2R, lane, c16, g, phase, sm.kacc, chunk * KC);
+            final_loop<D, RT, true>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.fin.nlse, out, a.s2,
+                                    log2R, lane, c16, g, phase, sm.v.fin.kacc, sm.v.fin.kaccs, chunk * KC);
         else
-            final_loop<D, RT, false>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.nlse, out, a.s2,
-                                     0.f, lane, c16, g, phase, sm.kacc, chunk * KC);
+            final_loop<D, RT, false>(Kh, kw, ngroups, N, clear_below, sm.lim, stA, stB, yr, sm.v.fin.nlse, out, a.s2,
+                                     0.f, lane, c16, g, phase, sm.v.fin.kacc, sm.v.fin.kaccs, chunk * KC);
         __syncthreads();  // the normalisers and limits are rewritten by the next group
     }
     // the item's scores, kept in LDS by the key loop, go out coalesced
     const int k0 = chunk * KC, nk = min(KC, N - k0);
-    for (int i = tid; i < nk; i += kThreads) out[k0 + i] = sm.kacc[i];
+    for (int i = tid; i < nk; i += kThreads) out[k0 + i] = sm.v.fin.kacc[i];
 }
 
 template <int D, int RT, bool MULTI>

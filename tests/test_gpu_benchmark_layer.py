@@ -1,14 +1,16 @@
 """GPU parity at the benchmark's full size: whole Qwen3-4B-shaped layers at
 32K tokens (B=16, Hkv=8, D=128, N=32768, R=144, budget 4096), evicted by the
 same calls bench.py times (score -> top-k -> compact on one workspace).
-Sampled heads are checked against the oracle, which computes them one by one;
-properties that hold at any size are checked on every head."""
+Every head of one layer is checked against the oracle (scores, kept set,
+and the selection and compaction in isolation, bit for bit); a second layer
+through the same workspace is checked on sampled heads; properties that hold
+at any size are checked on every head."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_util import assert_rows_match, assert_scores_close, compare_kept, dims_of, host, say
+from gpu_util import assert_rows_match, assert_scores_close, compare_kept, dims_of, host, raw_bits, say
 import paper_2609_04971_amd as bkv
 from paper_2609_04971_amd import synth
 
@@ -23,13 +25,57 @@ def _host_batches(x):
     return {k: host(v[BATCHES]) if k in per_batch else host(v) for k, v in x.items()}
 
 
-def test_benchmark_layers_sampled_heads():
+def test_benchmark_layer_all_heads():
+    # layer 0 of the benchmark: all 128 heads against the oracle
+    #  * scores element by element within 1e-3, kept under the tie-band rule;
+    #  * isolation, zero tolerance: the oracle's selection fed the GPU's own
+    #    scores reproduces the GPU's kept indices, and the oracle's compaction
+    #    fed the GPU's own kept indices reproduces the GPU's K and V
     w = synth.QWEN3_4B_32K
     d = dims_of(w)
     ws = bkv.workspace(d, bkv.OP_EVICT)
     scores = torch.empty(d.B, d.Hkv, d.N, device="cuda")
     kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
-    for layer in (0, 1):  # the second layer reuses the workspace, as the benchmark does
+    x = synth.make_layer(w, seed=100, device="cuda")
+    xh = {k: host(v) for k, v in x.items()}  # 2 GB of K and V before the eviction
+    say(f"benchmark layer 0, all heads: {d}")
+    bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+              rope_sin=x["rope_sin"])
+    bkv.topk(d, scores, kept)
+    bkv.compact(d, x["K"], x["V"], kept, ws)
+    torch.cuda.synchronize()
+    assert bkv.device_status(ws) == bkv.OK
+    s_all, k_all = host(scores).numpy(), host(kept).numpy()
+    assert not np.isnan(s_all).any() and np.all(s_all <= 1e-4)
+
+    say("  isolation: oracle top-k on the GPU's scores, all heads")
+    np.testing.assert_array_equal(oracle.topk(s_all.astype(np.float64), w.budget, w.W, 0), k_all)
+    say("  isolation: oracle compaction on the GPU's kept indices, all heads")
+    Kr, Vr = oracle.compact(xh["K"], xh["V"], k_all)
+    n = d.n_keep
+    assert np.array_equal(raw_bits(x["K"])[..., :n, :], Kr[..., :n, :].view(np.uint16)), "K differs"
+    assert np.array_equal(raw_bits(x["V"])[..., :n, :], Vr[..., :n, :].view(np.uint16)), "V differs"
+    del Kr, Vr
+
+    say("  oracle scores on all 128 heads")
+    s_ref, _ = oracle.score(xh["K"], xh["q_win"], xh["beacons"], xh["counts"], N=w.N, rope_cos=xh["rope_cos"],
+                            rope_sin=xh["rope_sin"], threads=16)
+    err = assert_scores_close(s_all, s_ref)
+    k_ref = oracle.topk(s_ref, w.budget, w.W, 0)
+    band, diff = compare_kept(k_all, k_ref, s_ref, w.N, w.W, 0, w.budget)
+    exact = int(np.all(k_all == k_ref, axis=-1).sum())
+    say(f"  max |score diff| {err:.2e}; tie band {band} keys, {diff} in-band differences; "
+        f"{exact}/{d.P} heads keep exactly the oracle's set")
+
+
+def test_benchmark_second_layer_sampled_heads():
+    # a second layer through the same workspace, as the benchmark runs it
+    w = synth.QWEN3_4B_32K
+    d = dims_of(w)
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    scores = torch.empty(d.B, d.Hkv, d.N, device="cuda")
+    kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
+    for layer in (0, 1):
         x = synth.make_layer(w, seed=100 + layer, device="cuda")
         xh = _host_batches(x)
         say(f"benchmark layer {layer}: {d}")
@@ -47,6 +93,8 @@ def test_benchmark_layers_sampled_heads():
         assert not np.isnan(s_all).any() and np.all(s_all <= 1e-4)
         assert np.all(np.diff(k_all, axis=-1) > 0)
         assert np.array_equal(k_all[..., -w.W:], np.broadcast_to(np.arange(w.N - w.W, w.N), k_all[..., -w.W:].shape))
+        if layer == 0:
+            continue  # all of layer 0 is checked above
 
         say(f"benchmark layer {layer}: oracle on {len(HEADS)} heads")
         ref = oracle.evict(xh["K"], xh["V"], xh["q_win"], xh["beacons"], xh["counts"], N=w.N, budget=w.budget,
@@ -63,6 +111,10 @@ def test_benchmark_layers_sampled_heads():
         V_gpu = host(x["V"][torch.as_tensor(bi), torch.as_tensor(hi)])
         assert_rows_match(K_gpu, ref["K"][li, hi], kg, kr, d.n_keep, "K")
         assert_rows_match(V_gpu, ref["V"][li, hi], kg, kr, d.n_keep, "V")
+        # every compacted row is the original row at the GPU's own index
+        for j, (b, h) in enumerate(HEADS):
+            src = raw_bits(xh["K"][b, h])[kg[j]]
+            assert np.array_equal(raw_bits(K_gpu[j])[: d.n_keep], src)
         del x
         torch.cuda.empty_cache()
 

@@ -144,3 +144,26 @@ def test_compact_repeated_hazard_patterns_deterministic():
             assert torch.equal(Kd.view(torch.int16), Kr), f"rep {rep} {name}"
             assert torch.equal(Kd.view(torch.int16), Vd.view(torch.int16))
     assert bkv.device_status(ws) == bkv.OK
+
+
+def test_compact_rejects_non_ascending_kept():
+    # kept[i] >= i and inside [0, N) everywhere, but one pair of head 1 is out
+    # of order: the segment holding it must move nothing and raise the device
+    # error, while head 0 compacts as usual
+    B, Hkv, N, D, budget = 1, 2, 512, 128, 128
+    d = bkv.dims(B=B, Hq=Hkv, Hkv=Hkv, D=D, N=N, W=0, C=1, budget=budget)
+    ws = bkv.workspace(d, bkv.OP_COMPACT)
+    kept = torch.arange(0, 2 * budget, 2, dtype=torch.int32).repeat(B * Hkv, 1).view(B, Hkv, budget).contiguous()
+    kept[0, 1, 10], kept[0, 1, 11] = int(kept[0, 1, 11]), int(kept[0, 1, 10])  # 22, 20
+    assert int(kept[0, 1, 11]) >= 11
+    K0 = _kv(B * Hkv, N, D, torch.bfloat16, seed=7).view(B, Hkv, N, D)
+    V0 = _kv(B * Hkv, N, D, torch.bfloat16, seed=8).view(B, Hkv, N, D)
+    Kd, Vd = K0.cuda(), V0.cuda()
+    say("compact non-ascending kept")
+    bkv.compact(d, Kd, Vd, kept.cuda(), ws)
+    assert bkv.device_status(ws) == bkv.ERR_DEVICE
+    Kr, Vr = oracle.compact(K0[:, :1], V0[:, :1], kept[:, :1].numpy())
+    np.testing.assert_array_equal(raw_bits(Kd[:, :1]), Kr.view(np.uint16))
+    np.testing.assert_array_equal(raw_bits(Vd[:, :1]), Vr.view(np.uint16))
+    # the first segment of head 1 (rows 0..63) holds the bad pair: untouched
+    np.testing.assert_array_equal(raw_bits(Kd[0, 1, :64]), raw_bits(K0[0, 1, :64]))
