@@ -23,7 +23,8 @@
  *
  * Conventions for every entry point:
  *   - Pointers to tensors are device pointers owned by the caller.  The
- *     library allocates nothing; scratch comes from the caller's workspace.
+ *     library allocates nothing; scratch comes from the caller's workspace
+ *     (bkv_evict_noalloc alone uses a fixed array of the library instead).
  *   - Work is enqueued on `stream` and is asynchronous; no call synchronises
  *     except bkv_device_status.
  *   - Arguments are validated on the host before anything is enqueued; on an
@@ -258,6 +259,31 @@ bkv_status bkv_evict_ex(const bkv_dims* d, int32_t flags, void* K, void* V, cons
                         const float* beacons, const int32_t* counts, const float* rope_cos,
                         const float* rope_sin, float scale, int32_t* kept, float* scores, float* row_lse,
                         void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- An eviction that allocates nothing ---------------------------------------
+ * For callers that cannot allocate device memory or pass a workspace: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  bkv_evict_ex's work (flags as there; scores, kept and row_lse
+ * optional outputs as there) with its workspace in a fixed array of this
+ * library, BKV_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU, held from the first
+ * call on that GPU until the process ends.  The call allocates nothing: no
+ * hipMalloc, hipFree or allocating library routine.  Every call on a GPU
+ * reuses that GPU's array, so calls that overlap in time on one GPU race:
+ * order them on one stream.  Each call first re-stamps and clears the
+ * array's control block with a fill kernel (no memset), so no
+ * initialisation call is needed and nothing carries over between calls.
+ *   device_status  optional device int32 output: BKV_OK, or BKV_ERR_DEVICE
+ *                  if a device-side check of this call tripped (the outputs
+ *                  are then unspecified); NULL to skip.
+ * Dims whose bkv_workspace_bytes(d, BKV_OP_EVICT) exceeds the array are
+ * BKV_ERR_WORKSPACE (checked on the host, nothing enqueued).  The first
+ * call on a GPU looks up the array's device address (hipGetSymbolAddress);
+ * failure there is BKV_ERR_HIP. */
+#define BKV_NOALLOC_SCRATCH_BYTES (32u << 20)
+bkv_status bkv_evict_noalloc(const bkv_dims* d, int32_t flags, void* K, void* V, const void* q_win,
+                             const float* beacons, const int32_t* counts, const float* rope_cos,
+                             const float* rope_sin, float scale, int32_t* kept, float* scores, float* row_lse,
+                             int32_t* device_status, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* bkv_status_string(bkv_status s);

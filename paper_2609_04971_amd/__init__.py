@@ -25,7 +25,7 @@ OP_BEACON_UPDATE, OP_SCORE, OP_TOPK, OP_COMPACT, OP_EVICT = range(5)
 EXPORTS = ("bkv_validate", "bkv_workspace_bytes", "bkv_workspace_init", "bkv_device_status",
            "bkv_beacon_update", "bkv_score", "bkv_topk", "bkv_compact", "bkv_evict",
            "bkv_score_ex", "bkv_evict_ex", "bkv_fps", "bkv_fps_gather", "bkv_status_string",
-           "bkv_abi_version", "bkv_compact_fill")
+           "bkv_abi_version", "bkv_compact_fill", "bkv_evict_noalloc")
 SCORE_MEAN, SCORE_CAUSAL = 1, 2
 
 
@@ -80,6 +80,7 @@ _SIGS = {
     "bkv_evict": ([_D, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_score_ex": ([_D, _I, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _S, _P], ctypes.c_int),
     "bkv_evict_ex": ([_D, _I, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _S, _P], ctypes.c_int),
+    "bkv_evict_noalloc": ([_D, _I, _P, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P], ctypes.c_int),
     "bkv_fps": ([_I] * 5 + [_P, _I, _P, _P], ctypes.c_int),
     "bkv_fps_gather": ([_I] * 5 + [_P, _I, _P, _I, _I, _P, _P, _P], ctypes.c_int),
     "bkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
@@ -267,6 +268,25 @@ def evict(d: Dims, K, V, q_win, beacons, counts, ws, kept=None, scores=None, row
         _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True), wp, wn,
         _stream())
     _check(st, "bkv_evict_ex")
+
+
+def evict_noalloc(d: Dims, K, V, q_win, beacons, counts, kept=None, scores=None, row_lse=None, rope_cos=None,
+                  rope_sin=None, scale: float = 0.0, mean: bool = False, causal: bool = False, status=None):
+    """evict() with the library's fixed device array as its workspace: no
+    workspace argument, nothing allocated.  status, an optional int32 tensor
+    of one element, receives the call's device status (OK or ERR_DEVICE)."""
+    rc, rs = _rope(rope_cos, rope_sin, d)
+    st = lib().bkv_evict_noalloc(
+        ctypes.byref(d), _flags(mean, causal), _ptr(K, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "K"),
+        _ptr(V, (d.B, d.Hkv, d.N_cap, d.D), _tdtype(d), "V"),
+        _ptr(q_win, (d.B, d.Hq, d.W, d.D), _tdtype(d), "q_win"),
+        _ptr(beacons, (d.B, d.Hkv, d.C, d.D), torch.float32, "beacons"),
+        _ptr(counts, (d.B, d.Hkv, d.C), torch.int32, "counts"), rc, rs, float(scale),
+        _ptr(kept, (d.B, d.Hkv, d.n_keep), torch.int32, "kept", optional=True),
+        _ptr(scores, (d.B, d.Hkv, d.N), torch.float32, "scores", optional=True),
+        _ptr(row_lse, (d.B, d.Hkv, d.C + d.G * d.W), torch.float32, "row_lse", optional=True),
+        _ptr(status, (1,), torch.int32, "status", optional=True), _stream())
+    _check(st, "bkv_evict_noalloc")
 
 
 # ---- Continual FPS -------------------------------------------------------------

@@ -248,6 +248,22 @@ bkv_status bkv_evict_ex(const bkv_dims* d, int32_t flags, void* K, void* V, cons
                         const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
                         int32_t* kept, float* scores, float* row_lse, void* ws, size_t ws_bytes,
                         hipStream_t stream) {
+    bkv_status st = bkv::evict_check(d, flags, K, V, q_win, beacons, counts, rope_cos, rope_sin, scale);
+    if (st != BKV_OK) return st;
+    if (empty_batch(d) || d->N == 0) return BKV_OK;
+    const WsLayout L = ws_layout(*d);
+    if (!ws || ws_bytes < L.evict_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
+    return bkv::evict_enqueue(d, flags, K, V, q_win, beacons, counts, rope_cos, rope_sin, scale, kept, scores,
+                              row_lse, ws, stream);
+}
+
+}  // extern "C"
+
+namespace bkv {
+
+bkv_status evict_check(const bkv_dims* d, int32_t flags, const void* K, const void* V, const void* q_win,
+                       const float* beacons, const int32_t* counts, const float* rope_cos, const float* rope_sin,
+                       float scale) {
     if (flags & ~(BKV_SCORE_MEAN | BKV_SCORE_CAUSAL)) return BKV_ERR_INVALID;
     bkv_status st = bkv_validate(d, BKV_OP_EVICT);
     if (st != BKV_OK) return st;
@@ -255,8 +271,13 @@ bkv_status bkv_evict_ex(const bkv_dims* d, int32_t flags, void* K, void* V, cons
     st = check_score_args(d, K, q_win, beacons, counts, rope_cos, rope_sin, scale);
     if (st != BKV_OK) return st;
     if (!V || !aligned16(V)) return BKV_ERR_INVALID;
+    return BKV_OK;
+}
+
+bkv_status evict_enqueue(const bkv_dims* d, int32_t flags, void* K, void* V, const void* q_win, const float* beacons,
+                         const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
+                         int32_t* kept, float* scores, float* row_lse, void* ws, hipStream_t stream) {
     const WsLayout L = ws_layout(*d);
-    if (!ws || ws_bytes < L.evict_end || !aligned16(ws)) return BKV_ERR_WORKSPACE;
     char* w = static_cast<char*>(ws);
     float* sc = scores ? scores : reinterpret_cast<float*>(w + L.scores);
     int32_t* kp = kept ? kept : reinterpret_cast<int32_t*>(w + L.kept);
@@ -267,6 +288,10 @@ bkv_status bkv_evict_ex(const bkv_dims* d, int32_t flags, void* K, void* V, cons
     if (e != hipSuccess) return BKV_ERR_HIP;
     return map_hip(launch_compact(*d, L, K, V, kp, ws, stream));
 }
+
+}  // namespace bkv
+
+extern "C" {
 
 static bkv_status check_fps_args(int32_t H, int32_t n, int32_t m, int32_t D, int32_t dtype, const void* q,
                                  int32_t q_rows) {

@@ -72,8 +72,17 @@ constexpr int kFastRowGroups = 8;
 
 WsLayout ws_layout(const bkv_dims& d);
 
+// ---- the whole eviction (bkv_evict_ex), split so that a caller can check the
+// arguments before it enqueues anything of its own -----------------------------
+bkv_status evict_check(const bkv_dims* d, int32_t flags, const void* K, const void* V, const void* q_win,
+                       const float* beacons, const int32_t* counts, const float* rope_cos, const float* rope_sin,
+                       float scale);
+// Arguments already checked, N > 0 and B > 0, ws holds ws_layout(d).evict_end bytes.
+bkv_status evict_enqueue(const bkv_dims* d, int32_t flags, void* K, void* V, const void* q_win, const float* beacons,
+                         const int32_t* counts, const float* rope_cos, const float* rope_sin, float scale,
+                         int32_t* kept, float* scores, float* row_lse, void* ws, hipStream_t stream);
+
 // ---- launches (enqueue only; arguments already validated) --------------------
-hipError_t launch_ws_init(void* ws, size_t ctl_bytes, int P, int budget, hipStream_t s);
 
 hipError_t launch_beacon_update(const bkv_dims& d, const void* q_new, int T, float* beacons,
                                 int32_t* counts, int32_t* assign, hipStream_t s);

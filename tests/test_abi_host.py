@@ -215,3 +215,17 @@ def test_compact_fill_rejects_before_launch():
     assert lib.bkv_compact_fill(ctypes.byref(big), fake, fake, fake, fake, None, 0, None) == bkv.ERR_SHAPE
     empty = good(B=0)
     assert lib.bkv_compact_fill(ctypes.byref(empty), None, None, None, None, None, 0, None) == bkv.OK
+
+
+def test_noalloc_rejects_dims_beyond_its_array():
+    # host-only: dims whose workspace exceeds the library's fixed array are
+    # refused before anything is enqueued (no device needed)
+    lib = bkv.lib()
+    big = good(B=64, N=65536, N_cap=65536, budget=8192)
+    assert lib.bkv_workspace_bytes(ctypes.byref(big), bkv.OP_EVICT) > (32 << 20)
+    st = lib.bkv_evict_noalloc(ctypes.byref(big), 0, None, None, None, None, None, None, None, 0.0, None, None,
+                               None, None, None)
+    assert st == bkv.ERR_INVALID  # NULL tensors are caught first
+    p = ctypes.c_void_p(16)  # any 16-byte aligned value: nothing is dereferenced on the host
+    st = lib.bkv_evict_noalloc(ctypes.byref(big), 0, p, p, p, p, p, None, None, 0.0, None, None, None, None, None)
+    assert st == bkv.ERR_WORKSPACE
