@@ -14,6 +14,9 @@ values drawn as follows:
   * queries are drawn around unit-norm cluster centroids per kv-head,
     q = sqrt(D) * (mu_k + sigma * xi), which gives attention logits of
     standard deviation ~1.5-2.5 like real attention (the sqrt(D) factor);
+    where configured the centroids drift on the unit sphere from one decode
+    step to the next (mu <- normalise(mu + drift * u), u a random unit
+    vector), so the recent window spans slowly moving clusters;
   * a fraction of recent queries are "revisits": a key among the first 1024
     tokens, rescaled to the query's norm (the paper's thought-revisiting
     queries, Section 3.1);
@@ -56,6 +59,7 @@ class Workload:
     head_scale: tuple = field(default=(1.0, 1.0))  # per-kv-head key scale ~ U(a, b)
     qscale: float | None = None             # None -> sqrt(D)
     rope_base: float = 1e6
+    drift: float = 0.0                      # centroid drift per decode step (0: static centroids)
 
     @property
     def G(self):
@@ -79,7 +83,7 @@ QWEN3_4B_32K = Workload("qwen3-4b-36L-N32768", B=16, Hq=32, Hkv=8, D=128, N=3276
 QWEN25_7B_16K = Workload("qwen2.5-7b-28L-N16384-gqa7", B=8, Hq=28, Hkv=4, D=128, N=16384, W=64, C=16,
                          budget=2048, layers=28, n_centroids=16, sigma=0.2, zipf=1.2, revisit_frac=0.0)
 LLAMA8B_64K = Workload("llama-8b-32L-N65536", B=4, Hq=32, Hkv=8, D=128, N=65536, W=128, C=32, budget=8192,
-                       layers=32, n_centroids=32, sigma=0.2, head_scale=(0.5, 2.0), revisit_frac=0.02)
+                       layers=32, n_centroids=32, sigma=0.2, head_scale=(0.5, 2.0), revisit_frac=0.02, drift=0.01)
 CONFIGS = {w.name: w for w in (TINY_FP32, QWEN3_4B_4K, QWEN3_4B_32K, QWEN25_7B_16K, LLAMA8B_64K)}
 
 
@@ -115,13 +119,33 @@ def _labels(w: Workload, shape, g, device):
 
 
 def _queries(w: Workload, mu, T: int, g, device):
-    """[B, Hq, T, D] fp32 around the kv-head's centroids."""
+    """[B, Hq, T, D] fp32 around the kv-head's centroids.  mu is [B, Hkv,
+    n_centroids, D] (the same centroids at every step) or [B, Hkv,
+    n_centroids, T, D] (step t's query around the centroids of step t)."""
     qs = w.qscale if w.qscale is not None else math.sqrt(w.D)
     lab = _labels(w, (w.B, w.Hq, T), g, device)
     kv = (torch.arange(w.Hq, device=device) // w.G).view(1, w.Hq, 1).expand(w.B, w.Hq, T)
     b = torch.arange(w.B, device=device).view(w.B, 1, 1).expand(w.B, w.Hq, T)
-    base = mu[b, kv, lab]
+    if mu.dim() == 5:
+        t = torch.arange(T, device=device).view(1, 1, T).expand(w.B, w.Hq, T)
+        base = mu[b, kv, lab, t]
+    else:
+        base = mu[b, kv, lab]
     return qs * (base + w.sigma * torch.randn(w.B, w.Hq, T, w.D, generator=g, device=device))
+
+
+def _drift_path(w: Workload, mu, steps: int, g, device):
+    """Centroids over `steps` decode steps, [B, Hkv, n_centroids, steps, D]:
+    the first step's are mu, and each step moves every centroid to
+    normalise(mu + drift * u) with u a random unit vector."""
+    out = torch.empty(*mu.shape[:3], steps, w.D, device=device)
+    cur = mu
+    for t in range(steps):
+        out[:, :, :, t] = cur
+        u = torch.randn(mu.shape, generator=g, device=device)
+        cur = cur + w.drift * u / u.norm(dim=-1, keepdim=True)
+        cur = cur / cur.norm(dim=-1, keepdim=True)
+    return out
 
 
 def make_layer(w: Workload, seed: int = 0, device="cpu", N_cap: int | None = None, v_random: bool = True):
@@ -144,7 +168,14 @@ def make_layer(w: Workload, seed: int = 0, device="cpu", N_cap: int | None = Non
     else:
         V = torch.empty_like(K)
     mu = _centroids(w, g, device)
-    q_win = _queries(w, mu, w.W, g, device)
+    if w.drift > 0:
+        # the recent queries sit at the last W steps before the current one;
+        # their centroids drift from step to step, and the current step's
+        # query (q_new) uses the centroids one step after the window's last
+        path = _drift_path(w, mu, w.W + 1, g, device)
+        q_win = _queries(w, path[:, :, :, : w.W], w.W, g, device)
+    else:
+        q_win = _queries(w, mu, w.W, g, device)
     if w.revisit_frac > 0 and w.W > 0:
         hit = torch.rand(w.B, w.Hq, w.W, generator=g, device=device) < w.revisit_frac
         span = max(1, min(w.revisit_span, w.N))
@@ -154,7 +185,7 @@ def make_layer(w: Workload, seed: int = 0, device="cpu", N_cap: int | None = Non
         kj = K[b, kv, j].float()
         rev = kj / kj.norm(dim=-1, keepdim=True) * q_win.norm(dim=-1, keepdim=True)
         q_win = torch.where(hit.unsqueeze(-1), rev, q_win)
-    q_new = _queries(w, mu, 1, g, device)
+    q_new = _queries(w, path[:, :, :, w.W:] if w.drift > 0 else mu, 1, g, device)
     counts = torch.randint(1, 65, (w.B, w.Hkv, w.C), generator=g, device=device, dtype=torch.int32)
     qs = w.qscale if w.qscale is not None else math.sqrt(w.D)
     cidx = torch.arange(w.C, device=device) % w.n_centroids
@@ -169,9 +200,12 @@ def make_layer(w: Workload, seed: int = 0, device="cpu", N_cap: int | None = Non
 
 
 def query_stream(w: Workload, T: int, seed: int = 0, device="cpu"):
-    """A stream of T pre-RoPE decode queries [B, Hq, T, D] around the centroids."""
+    """A stream of T pre-RoPE decode queries [B, Hq, T, D] around the
+    centroids (drifting from step to step when the workload's drift > 0)."""
     g = _gen(seed, device)
     mu = _centroids(w, g, device)
+    if w.drift > 0:
+        mu = _drift_path(w, mu, T, g, device)
     return _queries(w, mu, T, g, device).to(torch_dtype(w)).contiguous()
 
 
