@@ -814,6 +814,51 @@ __device__ __forceinline__ void stats_group(const uint16_t* st, int kb, const in
     });
 }
 
+// The same statistics with each lane's offset fixed: after an item's first
+// group every lane holds a finite offset ms per row tile (its running max,
+// or 0 where it has seen no key), and later groups only add exp2(y - ms).
+// A later key more than 127 (log2 units) above the offset overflows the sum
+// to +inf; the item then redoes its statistics with the running max.  The
+// offset is a key the lane has seen, so the sum is at least 1 and no key
+// that matters underflows.  Two VALU instructions and one exp2 per (row,
+// key) instead of about four and a bit.
+template <int D, int RT, bool TAIL>
+__device__ __forceinline__ void stats_group_fixed(const uint16_t* st, int kb, const int* lim,
+                                                  const Op<uint16_t, D>* yr, float s2, const float* nms, float* z,
+                                                  int c16, int g) {
+    Op<uint16_t, D> kop[2];
+    read_key_tile<D>(kop[0], st, 0, c16, g);
+    read_key_tile<D>(kop[1], st, 1, c16, g);
+    f32x4 acc[2][2];
+    auto issue = [&](int rt, f32x4* a) {
+        const int l = TAIL ? lim[rt * 16 + c16] : 0;  // this lane's row
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) a[t][v] = (!TAIL || kb + t * 16 + 4 * g + v <= l) ? 0.f : -INFINITY;
+            mma(a[t], kop[t], yr[rt]);  // rows = keys, columns = observation rows
+        }
+    };
+    issue(0, acc[0]);
+    dev::static_for<RT>([&](auto rt) {
+        if constexpr (rt + 1 < RT) issue(rt + 1, acc[(rt + 1) & 1]);
+        f32x4* a = acc[rt & 1];
+        const float nm = nms[rt];
+        float e[8];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) e[4 * t + v] = fast_exp2(__builtin_fmaf(a[t][v], s2, nm));
+        z[rt] += ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // three VALU
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    });
+}
+
 // Scores of one F item's staged group of 32 keys: per key the maximum over
 // rows (or the log of the mean weight), written straight out (64 contiguous
 // bytes per 16-key tile).  TAIL groups mask (key, row) pairs as in S.
@@ -972,30 +1017,68 @@ __device__ __forceinline__ void fast_stats(const Args& a, int h, int chunk, Fast
         }
         fill_limits<RT>(mk, rg * RT * 16, sm.lim);
         __syncthreads();
-        float m[RT], z[RT];
+        float m[RT], z[RT], nms[RT];
 #pragma unroll
         for (int i = 0; i < RT; ++i) {
             m[i] = -INFINITY;
             z[i] = 0.f;
         }
+        // the first group keeps a running max and fixes each lane's offset;
+        // the others add exp2(y - offset) only
+        auto fixed_body = [&](const uint16_t* st, int kb) {
+            if (kb + kFKG <= clear_below)
+                stats_group_fixed<D, RT, false>(st, kb, sm.lim, yr, s2, nms, z, c16, g);
+            else
+                stats_group_fixed<D, RT, true>(st, kb, sm.lim, yr, s2, nms, z, c16, g);
+        };
+        auto running_body = [&](const uint16_t* st, int kb) {
+            if (kb + kFKG <= clear_below)
+                stats_group<D, RT, false>(st, kb, sm.lim, yr, s2, m, z, c16, g);
+            else
+                stats_group<D, RT, true>(st, kb, sm.lim, yr, s2, m, z, c16, g);
+        };
 #pragma unroll 1
         for (int kg = 0; kg < ngroups; kg += 2) {
             const int kb = kw + kg * kFKG;
             wait_group<D>(kg + 1 < ngroups);
-            if (kb + kFKG <= clear_below)
-                stats_group<D, RT, false>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
-            else
-                stats_group<D, RT, true>(stA, kb, sm.lim, yr, s2, m, z, c16, g);
+            if (kg == 0) {
+                running_body(stA, kb);
+#pragma unroll
+                for (int i = 0; i < RT; ++i) {
+                    m[i] = (m[i] == -INFINITY) ? 0.f : m[i];
+                    nms[i] = -m[i];
+                }
+            } else {
+                fixed_body(stA, kb);
+            }
             if (kg + 2 < ngroups) issue_group<D>(Kh, kb + 2 * kFKG, N, stA, lane);
             if (kg + 1 < ngroups) {
                 wait_group<D>(kg + 2 < ngroups);
-                if (kb + 2 * kFKG <= clear_below)
-                    stats_group<D, RT, false>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
-                else
-                    stats_group<D, RT, true>(stB, kb + kFKG, sm.lim, yr, s2, m, z, c16, g);
+                fixed_body(stB, kb + kFKG);
                 if (kg + 3 < ngroups) issue_group<D>(Kh, kb + 3 * kFKG, N, stB, lane);
             }
         }
+        // a key far above its lane's offset overflowed a sum: redo this
+        // wave's statistics with the running max (not met on real data)
+        bool over = false;
+#pragma unroll
+        for (int i = 0; i < RT; ++i) over |= (z[i] == INFINITY);
+        if (__builtin_amdgcn_ballot_w64(over) != 0) {
+#pragma unroll
+            for (int i = 0; i < RT; ++i) {
+                m[i] = -INFINITY;
+                z[i] = 0.f;
+            }
+#pragma unroll 1
+            for (int kg = 0; kg < ngroups; ++kg) {
+                const int kb = kw + kg * kFKG;
+                issue_group<D>(Kh, kb, N, stA, lane);
+                wait_vmem<0>();
+                running_body(stA, kb);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RT; ++i) m[i] = (z[i] == 0.f) ? -INFINITY : m[i];  // a lane that saw no key
         // lanes sharing a row: g = 0..3, then waves
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {

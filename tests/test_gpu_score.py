@@ -132,3 +132,38 @@ def test_score_deterministic():
                   rope_sin=x["rope_sin"])
         outs.append(host(sc))
     assert torch.equal(outs[0], outs[1]) and torch.equal(outs[0], outs[2])
+
+
+@pytest.mark.parametrize("mean", [False, True])
+def test_score_key_far_above_its_lanes_first_keys(mean):
+    # a key whose logit for a row lies ~300 nats above everything else: it is
+    # not among the first keys a wave sees in its work item, so the row's
+    # running sum overflows against the offset taken from those first keys
+    # and the statistics are redone with a running max; scores and row
+    # normalisers must still match the oracle within 1e-3
+    import paper_2609_04971_amd as bkv
+    w = W("c9", B=2, Hq=8, Hkv=2, D=128, N=3000, W=8, C=4, budget=500)
+    x = synth.make_layer(w, seed=17, device="cpu")
+    K = x["K"].float()
+    for b in range(w.B):
+        for h in range(w.Hkv):
+            y = x["q_win"][b, h * w.G].float()[0]  # one recent row of the head
+            for j in (100, 1500 + 40 * h, 2999):
+                K[b, h, j] = 300.0 * np.sqrt(w.D) * y / y.norm() ** 2
+    x["K"] = K.to(torch.bfloat16).contiguous()
+    d = dims_of(w)
+    s_ref, lse_ref = oracle.score(x["K"], x["q_win"], x["beacons"], x["counts"], N=w.N, rope_cos=x["rope_cos"],
+                                  rope_sin=x["rope_sin"], threads=4, agg="mean" if mean else "max")
+    assert lse_ref[..., w.C].max() > 250.0, "the planted keys do not dominate their row"
+    xd = to_dev(x)
+    ws = bkv.workspace(d, bkv.OP_SCORE)
+    scores = torch.full((d.B, d.Hkv, d.N), float("nan"), device="cuda")
+    lse = torch.full((d.B, d.Hkv, d.C + d.G * d.W), float("nan"), device="cuda")
+    say(f"score with a dominant key, mean={mean}: {d}")
+    bkv.score(d, xd["K"], xd["q_win"], xd["beacons"], xd["counts"], scores, ws, row_lse=lse,
+              rope_cos=xd["rope_cos"], rope_sin=xd["rope_sin"], mean=mean)
+    torch.cuda.synchronize()
+    assert bkv.device_status(ws) == bkv.OK
+    err = assert_scores_close(host(scores).numpy(), s_ref)
+    assert_scores_close(host(lse).numpy(), lse_ref, "row_lse")
+    say(f"  max |diff| {err:.2e}")
