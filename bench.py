@@ -35,9 +35,10 @@ METRIC = "cached tokens scored+compacted/s per layer; eviction latency µs (Qwen
 
 # Measured HBM traffic of the score kernels on this workload (rocprofv3 FETCH_SIZE and
 # WRITE_SIZE, calibrated); used only while the kernel sources are unchanged since.
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "score_qwen3-4b-32k.md")
-SCORE_SOURCES = ("paper_2609_04971_amd/csrc/score.hip", "paper_2609_04971_amd/csrc/device_common.h",
-                 "paper_2609_04971_amd/csrc/internal.h", "include/bkv.h", "paper_2609_04971_amd/build.py")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "evict_qwen3-4b-32k.md")
+SCORE_SOURCES = ("paper_2609_04971_amd/csrc/score.hip", "paper_2609_04971_amd/csrc/evict_roles.h",
+                 "paper_2609_04971_amd/csrc/device_common.h", "paper_2609_04971_amd/csrc/internal.h",
+                 "include/bkv.h", "paper_2609_04971_amd/build.py")
 
 
 def score_source_digest() -> str:
@@ -126,7 +127,7 @@ def main():
     scores = torch.empty(d.B, d.Hkv, d.N, device=dev)
     kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device=dev)
     total = args.warmup + args.steps
-    EV = ["beacon", "score", "topk", "compact"]
+    EV = ["beacon", "evict"]
     events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in EV]
               for _ in range(total)]
 
@@ -137,15 +138,9 @@ def main():
         bkv.beacon_update(d, x["q_new"], x["beacons"], x["counts"])
         ev[0][1].record()
         ev[1][0].record()
-        bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
-                  rope_sin=x["rope_sin"])
+        bkv.evict(d, x["K"], x["V"], x["q_win"], x["beacons"], x["counts"], ws, kept=kept, scores=scores,
+                  rope_cos=x["rope_cos"], rope_sin=x["rope_sin"])
         ev[1][1].record()
-        ev[2][0].record()
-        bkv.topk(d, scores, kept)
-        ev[2][1].record()
-        ev[3][0].record()
-        bkv.compact(d, x["K"], x["V"], kept, ws)
-        ev[3][1].record()
 
     for i in range(args.warmup):
         step(i)
@@ -164,26 +159,27 @@ def main():
     per = {k: [events[i][j][0].elapsed_time(events[i][j][1]) * 1e3 for i in range(args.warmup, total)]
            for j, k in enumerate(EV)}
     avg_us = {k: statistics.mean(v) for k, v in per.items()}
-    evict_us = [per["score"][i] + per["topk"][i] + per["compact"][i] for i in range(args.steps)]
+    evict_us = per["evict"]
     rows = d.P * d.N
 
-    # ---- roofline of the dominant kernel (score) --------------------------
+    # ---- roofline of the dominant kernel: the fused eviction launch ----------
+    # algorithmic bytes: K read once, the scores written and read back by the
+    # selection, the kept indices written and read back by the compaction,
+    # every moved row of K and V read once and written once
     R = w.C + w.G * w.W
     es = 2
-    score_bytes = rows * (w.D * es + 4)          # K read once + one fp32 score written per cached row
-    score_flops = rows * 2 * R * w.D             # logits, counted once per (row, key)
-    score_s = avg_us["score"] * 1e-6
-    achieved = score_bytes / score_s / 1e9
+    evict_bytes = rows * w.D * es + 2 * rows * 4 + 2 * d.P * d.n_keep * 4 + moved * 4 * w.D * es
+    evict_flops = rows * 2 * R * w.D             # logits, counted once per (row, key)
+    evict_s = avg_us["evict"] * 1e-6
+    achieved = evict_bytes / evict_s / 1e9
+    evict_med = statistics.median(evict_us)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
-                "kernel": "score launch: rows_kernel<128> + fast_score_kernel<128, 9>",
-                "algorithmic_bytes": score_bytes,
-                "mfma_tflops": round(score_flops / score_s / 1e12, 1),
-                "mfma_frac": round(score_flops / score_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}
-    # whole eviction against HBM: K read once, scores and indices written and
-    # read back, every moved row of K and V read and written once
-    evict_bytes = rows * w.D * es + 2 * rows * 4 + 2 * d.P * d.n_keep * 4 + moved * 4 * w.D * es
-    evict_med = statistics.median(evict_us)
+                "kernel": "eviction launch: rows_kernel<128> + evict_kernel<128, 9, false>",
+                "algorithmic_bytes": evict_bytes, "moved_rows": moved,
+                "launch_us_mean": round(avg_us["evict"], 1),
+                "mfma_tflops": round(evict_flops / evict_s / 1e12, 1),
+                "mfma_frac": round(evict_flops / evict_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}
 
     out = {
         "metric": METRIC,
@@ -206,6 +202,8 @@ def main():
         "roofline": roofline,
         "setup_s": round(gen_s, 1),
     }
+    score_bytes = rows * (w.D * es + 4)  # K read once + one fp32 score written per cached row
+    out["stages"] = stages_measure(w, dev)
     if not args.no_fps:
         out["score_options"] = score_options_measure(d, layers, scores, ws, score_bytes)
     del layers
@@ -227,6 +225,59 @@ def main():
     out["roofline"]["frac_of_measured_copy"] = round(out["roofline"]["achieved"] / bw["copy_GBs"], 4)
     out["evict_hbm"]["frac_of_measured_copy"] = round(out["evict_hbm"]["achieved_GBs"] / bw["copy_GBs"], 4)
     print(json.dumps(out), flush=True)
+
+
+def stages_measure(w, dev, reps=5):
+    """The eviction's stages of one 32K layer as separate calls (bkv_score,
+    bkv_topk, bkv_compact) next to the fused bkv_evict, each on a fresh copy
+    of the same generated layer (the copy is not timed), HIP events on the
+    launch stream; medians of `reps`.  The fused launch overlaps the
+    selection and compaction of earlier heads with the scoring of later
+    ones; the chained calls run them one after the other."""
+    import torch
+
+    import paper_2609_04971_amd as bkv
+    from paper_2609_04971_amd import synth
+
+    d = bkv.dims(B=w.B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, N=w.N, W=w.W, C=w.C, budget=w.budget, dtype=w.dtype)
+    x = synth.make_layer(w, seed=999, device=dev)
+    K0, V0 = x["K"].clone(), x["V"].clone()
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device=dev)
+    scores = torch.empty(d.B, d.Hkv, d.N, device=dev)
+    t = {"score": [], "topk": [], "compact": [], "chained": [], "fused": []}
+    for r in range(reps + 1):
+        x["K"].copy_(K0)
+        x["V"].copy_(V0)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record()
+        bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+                  rope_sin=x["rope_sin"])
+        e[1].record()
+        bkv.topk(d, scores, kept)
+        e[2].record()
+        bkv.compact(d, x["K"], x["V"], kept, ws)
+        e[3].record()
+        x["K"].copy_(K0)
+        x["V"].copy_(V0)
+        torch.cuda.synchronize()
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record()
+        bkv.evict(d, x["K"], x["V"], x["q_win"], x["beacons"], x["counts"], ws, kept=kept, scores=scores,
+                  rope_cos=x["rope_cos"], rope_sin=x["rope_sin"])
+        f1.record()
+        torch.cuda.synchronize()
+        if r:
+            t["score"].append(e[0].elapsed_time(e[1]) * 1e3)
+            t["topk"].append(e[1].elapsed_time(e[2]) * 1e3)
+            t["compact"].append(e[2].elapsed_time(e[3]) * 1e3)
+            t["chained"].append(e[0].elapsed_time(e[3]) * 1e3)
+            t["fused"].append(f0.elapsed_time(f1) * 1e3)
+    assert bkv.device_status(ws) == bkv.OK
+    del x, K0, V0, ws, kept, scores
+    torch.cuda.empty_cache()
+    return {k + "_us": round(statistics.median(v), 1) for k, v in t.items()}
 
 
 def score_options_measure(d, layers, scores, ws, score_bytes, reps=6):

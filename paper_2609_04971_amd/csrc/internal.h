@@ -34,6 +34,12 @@ enum HeadWord : int {
     kHcReady = 3,     // score: the head's row normalisers are published
     kHcCpTicket = 4,  // compaction: work ticket within the head
     kHcCpDone = 5,    // compaction: segments of the head finished
+    // the fused eviction launch (score, select and compaction work items of
+    // every head under the score ticket)
+    kHcFcDone = 6,    // fused: compaction segments of the head finished
+    kHcFDone = 7,     // fused: final-score items of the head finished
+    kHcScReady = 8,   // fused: the head's scores are all stored
+    kHcKept = 9,      // fused: the head's kept indices are stored
     kHcWords = 32
 };
 
@@ -91,6 +97,15 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
                         const float* beacons, const int32_t* counts, const float* rope_cos,
                         const float* rope_sin, float scale, float* scores, float* row_lse,
                         void* ws, hipStream_t s);
+
+// The whole eviction in one launch (score, select and compact work items
+// under one per-head ticket); only where evict_fusable(L) (the bf16 fast
+// path).  kept and scores are required (the workspace's own may be passed).
+bool evict_fusable(const WsLayout& L);
+hipError_t launch_evict_fused(const bkv_dims& d, const WsLayout& L, int flags, void* K, void* V, const void* q_win,
+                              const float* beacons, const int32_t* counts, const float* rope_cos,
+                              const float* rope_sin, float scale, float* scores, float* row_lse, int32_t* kept,
+                              void* ws, hipStream_t s);
 
 hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hipStream_t s);
 hipError_t launch_compact_fill(const bkv_dims& d, void* K, void* V, const int32_t* kept, int32_t* src_of, void* ws,

@@ -37,8 +37,10 @@
 // accumulator starts at -lse2_r / s2, so the MFMA yields l_rj - lse_r (up
 // to the factor s2) directly and the epilogue is one max per element.
 #include <math.h>
+#include <string.h>
 
 #include "device_common.h"
+#include "evict_roles.h"
 #include "internal.h"
 
 namespace bkv {
@@ -88,6 +90,19 @@ struct Args {
     float s2ln2;  // s2 * ln(2): log2-units-of-raw-dot -> natural log
     int mean;     // aggregate by the mean over rows (else the max)
     int causal;   // recent row w sees keys up to N - W + w only
+    int tickets;  // work items per head (the ticket limit)
+    // the fused eviction launch (evict_kernel): after each head's score items
+    // one selection item and nsegF compaction items of roles::kSegF rows
+    int fused;
+    char* Kc;       // K and V, compacted in place
+    char* Vc;
+    int32_t* kept;  // [P][n_keep]
+    int* cflags;    // [P][nseg_cap] compaction read-done flags
+    int n_prefix, n_keep, nsegF, nseg_cap, lag2, lag3;
+    // grid regions of the fused launch: slots [rs[i], rs[i+1]) hold rper[i]
+    // workgroups each, starting at workgroup rb[i]
+    int nreg;
+    int rs[8], rb[8], rper[8];
 };
 
 // Which (key, row) pairs enter the scores: keys at or past N never do, and
@@ -563,7 +578,7 @@ __device__ __forceinline__ bool complete_ticket(const Args& a, const TicketReq& 
     if (threadIdx.x == 0) {
         int ok = r.hdr[kHdrMagic] == kWsMagic && (int)r.hdr[kHdrP] == a.P && (int)r.hdr[kHdrBudget] == a.budget;
         *s_ticket = r.t;
-        if (ok && r.t >= 2 * a.nch) ok = 0;  // control line was not clear: do nothing
+        if (ok && r.t >= a.tickets) ok = 0;  // control line was not clear: do nothing
         if (!ok) dev::raise_error(a.hdr, kErrStamp);
         *s_ok = ok;
     }
@@ -575,12 +590,20 @@ __device__ __forceinline__ bool complete_ticket(const Args& a, const TicketReq& 
 // this for all heads in a kernel of its own, before any work item takes a
 // ticket, so work items never wait at the end to find the head's last one.
 __device__ __forceinline__ void reset_head_control(const Args& a, int h) {
+    int* hc = a.hctl + (size_t)h * kHcWords;
     if (threadIdx.x == 0) {
-        int* hc = a.hctl + (size_t)h * kHcWords;
         dev::st_flag(hc + kHcScTicket, 0);
         dev::st_flag(hc + kHcP1Count, 0);
         dev::st_flag(hc + kHcReady, 0);
+        if (a.fused) {
+            dev::st_flag(hc + kHcFcDone, 0);
+            dev::st_flag(hc + kHcFDone, 0);
+            dev::st_flag(hc + kHcScReady, 0);
+            dev::st_flag(hc + kHcKept, 0);
+        }
     }
+    if (a.fused)
+        for (int i = threadIdx.x; i < a.nsegF; i += blockDim.x) dev::st_flag(a.cflags + (size_t)h * a.nseg_cap + i, 0);
 }
 
 __global__ void reset_control_kernel(Args a) {
@@ -1180,7 +1203,20 @@ __device__ __forceinline__ void fast_final(const Args& a, int h, int chunk, Fast
     }
     // the item's scores, kept in LDS by the key loop, go out coalesced
     const int k0 = chunk * KC, nk = min(KC, N - k0);
-    for (int i = tid; i < nk; i += kThreads) out[k0 + i] = sm.v.fin.kacc[i];
+    if (!a.fused) {
+        for (int i = tid; i < nk; i += kThreads) out[k0 + i] = sm.v.fin.kacc[i];
+        return;
+    }
+    // fused launch: the head's selection item (maybe on another XCD) reads
+    // them, so they are written through coherently and counted in; the last
+    // item of the head marks its scores complete
+    for (int i = tid; i < nk; i += kThreads) dev::st_coherent(out + k0 + i, sm.v.fin.kacc[i]);
+    dev::wait_all_memory();
+    __syncthreads();
+    if (tid == 0) {
+        int* hc = a.hctl + (size_t)h * kHcWords;
+        if (dev::fetch_add_relaxed(hc + kHcFDone, 1) == a.nch - 1) dev::st_flag(hc + kHcScReady, 1);
+    }
 }
 
 template <int D, int RT, bool MULTI>
@@ -1204,13 +1240,123 @@ __global__ __launch_bounds__(kThreads, 2) void fast_score_kernel(Args a) {
         fast_final<D, RT, MULTI>(a, h, ticket - a.nch, sm, sa, sb, yr, &s_flag);
 }
 
+// ---- the fused eviction: score, select and compact under one ticket ------
+//
+// Each head's work items, in ticket order: nch S items, nch F items, one
+// selection item (once every F item of the head has stored its scores) and
+// nsegF compaction items (once the head's kept indices are stored).  Every
+// wait is on lower tickets of the same head, which have started and never
+// wait on higher ones, so the launch cannot deadlock whatever the
+// residency.  The grid lists a head's selection and compaction workgroups
+// lag2 heads after its first, so that the HBM-bound compaction of earlier
+// heads runs while later heads are being scored.
+
+// Workgroup -> head in the fused grid: slot s holds the S workgroups of head
+// s (s < P), the F workgroups of head s - lag (lag <= s < P + lag), the
+// selection workgroup of head s - lag2 and the compaction workgroups of
+// head s - lag3, in that order; the host lists the slot ranges of equal
+// size.  Workgroups that start early only wait (holding their slot), so
+// each kind comes a few machine-fulls after what it needs.
+__device__ __forceinline__ int head_of_block_fused(const Args& a, int b) {
+    int i = 0;
+    while (i + 1 < a.nreg && b >= a.rb[i + 1]) ++i;
+    const int per = a.rper[i];
+    const int s = a.rs[i] + (b - a.rb[i]) / per;
+    int r = (b - a.rb[i]) % per;
+    if (s < a.P) {
+        if (r < a.nch) return s;
+        r -= a.nch;
+    }
+    if (s >= a.lag && s < a.P + a.lag) {
+        if (r < a.nch) return s - a.lag;
+        r -= a.nch;
+    }
+    if (s >= a.lag2 && s < a.P + a.lag2) {
+        if (r < 1) return s - a.lag2;
+    }
+    return s - a.lag3;
+}
+
+template <int D, int RT, bool MULTI>
+__global__ __launch_bounds__(kThreads, 2) void evict_kernel(Args a) {
+    __shared__ FastSmem sm;
+    __shared__ StageBuf<D> sa;
+    __shared__ StageBuf<D> sb;
+    __shared__ int s_ticket, s_ok, s_flag;
+    const int h = head_of_block_fused(a, blockIdx.x);
+    const TicketReq req = request_ticket(a, h);
+    if (!complete_ticket(a, req, &s_ticket, &s_ok)) return;
+    const int ticket = __builtin_amdgcn_readfirstlane(s_ticket);
+    if (ticket < 2 * a.nch) {
+        Op<uint16_t, D> yr[RT];
+        if (!MULTI) load_rows<D, RT>(a, h, 0, yr, threadIdx.x & 63);
+        if (ticket < a.nch)
+            fast_stats<D, RT, MULTI>(a, h, ticket, sm, sa, sb, yr, &s_flag);
+        else
+            fast_final<D, RT, MULTI>(a, h, ticket - a.nch, sm, sa, sb, yr, &s_flag);
+        return;
+    }
+    const int tid = threadIdx.x;
+    int* hc = a.hctl + (size_t)h * kHcWords;
+    if (ticket == 2 * a.nch) {
+        // selection: every F item of the head has stored its scores
+        if (tid == 0) {
+            s_flag = dev::wait_flag(hc + kHcScReady);
+            if (!s_flag) dev::raise_error(a.hdr, kErrScoreWait);
+        }
+        __syncthreads();
+        constexpr int BINS = sizeof(StageBuf<D>) >= sizeof(roles::SelLds<4096>) ? 4096 : 2048;
+        static_assert(sizeof(roles::SelLds<BINS>) <= sizeof(StageBuf<D>), "selection LDS");
+        if (s_flag)
+            roles::select_item<BINS>(a.scores + (size_t)h * a.N, a.kept + (size_t)h * a.n_keep, a.N, a.budget, a.W,
+                                     a.n_prefix, *reinterpret_cast<roles::SelLds<BINS>*>(&sa));
+        dev::wait_all_memory();
+        __syncthreads();
+        if (tid == 0) dev::st_flag(hc + kHcKept, s_flag ? 1 : 2);  // 2: no valid kept set
+        return;
+    }
+    // compaction segment: the head's kept indices are stored
+    const int seg = ticket - 2 * a.nch - 1;
+    if (tid == 0) {
+        s_flag = dev::wait_flag(hc + kHcKept) && dev::ld_flag(hc + kHcKept) == 1;
+        if (!s_flag) dev::raise_error(a.hdr, kErrCompactWait);
+    }
+    __syncthreads();
+    int* lds = reinterpret_cast<int*>(&sa);
+    int* flags = a.cflags + (size_t)h * a.nseg_cap;
+    bool ok = true;
+    if (s_flag) {
+        const size_t hs = (size_t)a.N_cap * D * 2;
+        ok = roles::compact_item<D * 2>(a.Kc + (size_t)h * hs, a.Vc + (size_t)h * hs, a.kept + (size_t)h * a.n_keep,
+                                        flags, seg, a.n_keep, a.N, lds, lds + roles::kSegF, a.hdr);
+    } else if (tid == 0) {
+        dev::st_flag(flags + seg, 1);  // lower-ticket waits of later segments end
+    }
+    if (!ok && tid == 0) dev::raise_error(a.hdr, kErrBadIndex);
+    // the head's last segment leaves its flags clear for later launches
+    __syncthreads();
+    if (tid == 0) s_ok = dev::fetch_add_relaxed(hc + kHcFcDone, 1) == a.nsegF - 1;
+    __syncthreads();
+    if (s_ok) {
+        for (int i = tid; i < a.nsegF; i += kThreads) dev::st_flag(flags + i, 0);
+        if (tid == 0) dev::st_flag(hc + kHcFcDone, 0);
+    }
+}
+
 template <int D, int RT>
 hipError_t launch_fast_rt(const Args& a, hipStream_t s) {
     hipLaunchKernelGGL((rows_kernel<D>), dim3(a.P), dim3(kThreads), 0, s, a);
-    if (a.R_pad_max > RT * 16)
+    const bool multi = a.R_pad_max > RT * 16;
+    if (a.fused) {
+        if (multi)
+            hipLaunchKernelGGL((evict_kernel<D, RT, true>), dim3(a.total), dim3(kThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((evict_kernel<D, RT, false>), dim3(a.total), dim3(kThreads), 0, s, a);
+    } else if (multi) {
         hipLaunchKernelGGL((fast_score_kernel<D, RT, true>), dim3(a.total), dim3(kThreads), 0, s, a);
-    else
+    } else {
         hipLaunchKernelGGL((fast_score_kernel<D, RT, false>), dim3(a.total), dim3(kThreads), 0, s, a);
+    }
     return hipGetLastError();
 }
 
@@ -1238,12 +1384,43 @@ hipError_t launch_t(const Args& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const void* K, const void* q_win,
-                        const float* beacons, const int32_t* counts, const float* rope_cos,
-                        const float* rope_sin, float scale, float* scores, float* row_lse, void* ws,
-                        hipStream_t s) {
+namespace {
+
+// Grid of the fused launch: the slot ranges of equal composition (see
+// head_of_block_fused).
+void fused_regions(Args& a) {
+    const int P = a.P;
+    int bp[8] = {0, a.lag, a.lag2, a.lag3, P, P + a.lag, P + a.lag2, P + a.lag3};
+    for (int i = 1; i < 8; ++i)  // sort the breakpoints
+        for (int j = i; j > 0 && bp[j] < bp[j - 1]; --j) {
+            const int t = bp[j];
+            bp[j] = bp[j - 1];
+            bp[j - 1] = t;
+        }
+    a.nreg = 0;
+    int b = 0;
+    for (int i = 0; i + 1 < 8; ++i) {
+        const int x = bp[i], y = bp[i + 1];
+        if (x >= y) continue;
+        const int per = (x < P ? a.nch : 0) + (x >= a.lag && x < P + a.lag ? a.nch : 0) +
+                        (x >= a.lag2 && x < P + a.lag2 ? 1 : 0) + (x >= a.lag3 && x < P + a.lag3 ? a.nsegF : 0);
+        if (per == 0) continue;
+        a.rs[a.nreg] = x;
+        a.rb[a.nreg] = b;
+        a.rper[a.nreg] = per;
+        ++a.nreg;
+        b += per * (y - x);
+    }
+    a.total = b;
+}
+
+hipError_t launch_score_impl(const bkv_dims& d, const WsLayout& L, int flags, const void* K, void* V,
+                             const void* q_win, const float* beacons, const int32_t* counts, const float* rope_cos,
+                             const float* rope_sin, float scale, float* scores, float* row_lse, int32_t* kept,
+                             void* ws, hipStream_t s) {
     char* w = static_cast<char*>(ws);
     Args a;
+    memset(&a, 0, sizeof a);
     a.K = K;
     a.qwin = q_win;
     a.beacons = beacons;
@@ -1282,6 +1459,25 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
     int lag = (4 * cus + 2 * L.nch - 1) / (2 * L.nch);
     a.lag = lag < 1 ? 1 : (lag > L.P ? L.P : lag);
     a.total = 2 * L.P * L.nch;
+    a.tickets = 2 * L.nch;
+    if (V) {  // the fused eviction (fast path only)
+        a.fused = 1;
+        a.Kc = static_cast<char*>(const_cast<void*>(K));
+        a.Vc = static_cast<char*>(V);
+        a.kept = kept;
+        a.cflags = reinterpret_cast<int*>(w + L.cflags);
+        a.n_prefix = d.n_prefix;
+        a.n_keep = d.N < d.budget ? d.N : d.budget;
+        a.nsegF = (a.n_keep + roles::kSegF - 1) / roles::kSegF;
+        a.nseg_cap = L.nseg;
+        a.tickets = 2 * L.nch + 1 + a.nsegF;
+        // the selection about two machine-fulls of workgroups after the
+        // head's F items, the compaction about four more after the selection
+        const int step = (4 * cus + a.tickets - 1) / a.tickets;
+        a.lag2 = a.lag + step > L.P ? L.P : a.lag + step;
+        a.lag3 = a.lag2 + 2 * step > L.P ? L.P : a.lag2 + 2 * step;
+        fused_regions(a);
+    }
     const float sc = (scale == 0.0f) ? (float)(1.0 / sqrt((double)d.D)) : scale;
     a.s2 = sc * 1.4426950408889634f;
     a.s2ln2 = a.s2 * 0.69314718055994531f;
@@ -1293,11 +1489,32 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
         a.rmeta = reinterpret_cast<int*>(w + L.rmeta);
         return d.D == 128 ? launch_fast<128>(a, L.rtg, s) : launch_fast<64>(a, L.rtg, s);
     }
+    if (a.fused) return hipErrorNotSupported;  // the caller checks evict_fusable first
     const bool k4 = L.kgn == 4;  // 1024-key items (else 256)
     if (bf && d.D == 128) return k4 ? launch_t<uint16_t, 128, 4>(a, s) : launch_t<uint16_t, 128, 1>(a, s);
     if (bf) return k4 ? launch_t<uint16_t, 64, 4>(a, s) : launch_t<uint16_t, 64, 1>(a, s);
     if (d.D == 128) return k4 ? launch_t<float, 128, 4>(a, s) : launch_t<float, 128, 1>(a, s);
     return k4 ? launch_t<float, 64, 4>(a, s) : launch_t<float, 64, 1>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const void* K, const void* q_win,
+                        const float* beacons, const int32_t* counts, const float* rope_cos,
+                        const float* rope_sin, float scale, float* scores, float* row_lse, void* ws,
+                        hipStream_t s) {
+    return launch_score_impl(d, L, flags, K, nullptr, q_win, beacons, counts, rope_cos, rope_sin, scale, scores,
+                             row_lse, nullptr, ws, s);
+}
+
+bool evict_fusable(const WsLayout& L) { return L.rtg > 0; }
+
+hipError_t launch_evict_fused(const bkv_dims& d, const WsLayout& L, int flags, void* K, void* V, const void* q_win,
+                              const float* beacons, const int32_t* counts, const float* rope_cos,
+                              const float* rope_sin, float scale, float* scores, float* row_lse, int32_t* kept,
+                              void* ws, hipStream_t s) {
+    return launch_score_impl(d, L, flags, K, V, q_win, beacons, counts, rope_cos, rope_sin, scale, scores, row_lse,
+                             kept, ws, s);
 }
 
 }  // namespace bkv

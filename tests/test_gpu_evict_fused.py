@@ -1,0 +1,119 @@
+"""The fused eviction launch (bkv_evict on the bf16 fast path: score,
+selection and compaction work items of every head under one ticket) against
+the oracle and against the chained entry points.
+
+Checks per case:
+  * scores within 1e-3 of the oracle;
+  * isolation, zero tolerance: the oracle's selection fed the GPU's own
+    scores gives exactly the GPU's kept indices, and the oracle's compaction
+    fed the GPU's kept indices gives exactly the GPU's K and V;
+  * bkv_score -> bkv_topk -> bkv_compact on a copy give the same kept
+    indices and the same K and V bit for bit.
+Cases cover ragged N, D = 64, the prefix, W = 0, N <= budget, rows in several
+register groups, the scoring options, and layers whose keys repeat a few
+rows only, so that scores tie in bulk (the selection's exact radix path and
+its tie ranking by index)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import assert_scores_close, dims_of, host, raw_bits, say
+import paper_2609_04971_amd as bkv
+from paper_2609_04971_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+W = synth.Workload
+CASES = {
+    "ragged": W("f1", B=2, Hq=8, Hkv=2, D=128, N=1001, W=8, C=4, budget=300, revisit_frac=0.1),
+    "prefix": W("f2", B=2, Hq=8, Hkv=2, D=128, N=3000, W=16, C=8, budget=700, n_prefix=5),
+    "d64-g7": W("f3", B=1, Hq=14, Hkv=2, D=64, N=2100, W=5, C=3, budget=512, n_centroids=3),
+    "no-window": W("f4", B=1, Hq=8, Hkv=2, D=128, N=1500, W=0, C=8, budget=200),
+    "n-below-budget": W("f5", B=1, Hq=4, Hkv=2, D=128, N=90, W=8, C=4, budget=100),
+    "n-equals-budget": W("f6", B=1, Hq=4, Hkv=2, D=128, N=256, W=8, C=4, budget=256),
+    "two-row-groups": W("f7", B=1, Hq=14, Hkv=2, D=128, N=2000, W=24, C=16, budget=300, n_centroids=16),
+    "many-heads": W("f8", B=16, Hq=32, Hkv=8, D=128, N=8192, W=32, C=16, budget=1024, revisit_frac=0.05),
+    "long-64k": W("f9", B=1, Hq=8, Hkv=2, D=128, N=65536, W=128, C=32, budget=8192, revisit_frac=0.02),
+}
+
+
+def _evict_both(d, x, mean=False, causal=False):
+    """Fused eviction on x and the chained calls on a copy; returns both."""
+    opt = dict(rope_cos=x["rope_cos"], rope_sin=x["rope_sin"], mean=mean, causal=causal)
+    K2, V2 = x["K"].clone(), x["V"].clone()
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    kept = torch.full((d.B, d.Hkv, d.n_keep), -1, dtype=torch.int32, device="cuda")
+    scores = torch.full((d.B, d.Hkv, d.N), float("nan"), device="cuda")
+    bkv.evict(d, x["K"], x["V"], x["q_win"], x["beacons"], x["counts"], ws, kept=kept, scores=scores, **opt)
+    assert bkv.device_status(ws) == bkv.OK
+    ws2 = bkv.workspace(d, bkv.OP_EVICT)
+    kept2 = torch.full_like(kept, -1)
+    scores2 = torch.empty_like(scores)
+    bkv.score(d, K2, x["q_win"], x["beacons"], x["counts"], scores2, ws2, **opt)
+    bkv.topk(d, scores2, kept2)
+    bkv.compact(d, K2, V2, kept2, ws2)
+    assert bkv.device_status(ws2) == bkv.OK
+    return (kept, scores), (kept2, scores2, K2, V2)
+
+
+def _check(w, x0, d, mean=False, causal=False, seed_note=""):
+    xd = {k: v.cuda() for k, v in x0.items()}
+    (kept, scores), (kept2, scores2, K2, V2) = _evict_both(d, xd, mean, causal)
+    s_gpu, k_gpu = host(scores).numpy(), host(kept).numpy()
+    heads = None if w.P <= 16 else [(b, h) for b in (0, w.B - 1) for h in (0, w.Hkv - 1)]
+    s_ref, _ = oracle.score(x0["K"], x0["q_win"], x0["beacons"], x0["counts"], N=w.N, rope_cos=x0["rope_cos"],
+                            rope_sin=x0["rope_sin"], heads=heads, threads=8, agg="mean" if mean else "max",
+                            causal=causal)
+    sel = (slice(None),) if heads is None else tuple(np.array(heads).T)
+    err = assert_scores_close(s_gpu[sel], s_ref[sel])
+    # isolation checks on every head
+    np.testing.assert_array_equal(oracle.topk(s_gpu.astype(np.float64), w.budget, w.W, w.n_prefix), k_gpu)
+    Kr, Vr = oracle.compact(x0["K"], x0["V"], k_gpu)
+    n = d.n_keep
+    assert np.array_equal(raw_bits(xd["K"])[..., :n, :], Kr[..., :n, :].view(np.uint16)), "K differs"
+    assert np.array_equal(raw_bits(xd["V"])[..., :n, :], Vr[..., :n, :].view(np.uint16)), "V differs"
+    assert np.array_equal(raw_bits(xd["K"])[..., n:, :], raw_bits(x0["K"])[..., n:, :]), "rows past n moved"
+    # the chained entry points agree bit for bit
+    np.testing.assert_array_equal(host(scores2).numpy(), s_gpu)
+    np.testing.assert_array_equal(host(kept2).numpy(), k_gpu)
+    assert torch.equal(K2.view(torch.int16), xd["K"].view(torch.int16))
+    assert torch.equal(V2.view(torch.int16), xd["V"].view(torch.int16))
+    say(f"  {seed_note}max |score diff| {err:.2e}")
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_fused_evict(name):
+    w = CASES[name]
+    big = w.P * w.N > 1 << 20
+    x = synth.make_layer(w, seed=71, device="cuda" if big else "cpu")
+    x = {k: host(v) for k, v in x.items()}
+    d = dims_of(w)
+    say(f"fused evict {name} {d}")
+    _check(w, x, d)
+
+
+@pytest.mark.parametrize("mean,causal", [(True, False), (False, True), (True, True)])
+def test_fused_evict_options(mean, causal):
+    w = CASES["prefix"]
+    x = synth.make_layer(w, seed=72, device="cpu")
+    d = dims_of(w)
+    say(f"fused evict mean={mean} causal={causal} {d}")
+    _check(w, x, d, mean, causal)
+
+
+@pytest.mark.parametrize("distinct", [1, 3, 40])
+def test_fused_evict_bulk_ties(distinct):
+    # keys repeat `distinct` rows only: scores tie in bulk, so the threshold
+    # value is shared by many candidates (one distinct row: every candidate
+    # ties) and the kept ones among equals must be the lowest indices
+    w = W("f10", B=2, Hq=8, Hkv=2, D=128, N=4100, W=16, C=4, budget=900, n_prefix=2)
+    x = synth.make_layer(w, seed=73, device="cpu")
+    g = torch.Generator().manual_seed(74)
+    pick = torch.randint(0, distinct, (w.B, w.Hkv, w.N), generator=g)
+    K = x["K"]
+    rows = K[:, :, :distinct].clone()
+    K[:] = torch.gather(rows, 2, pick.unsqueeze(-1).expand(-1, -1, -1, w.D))
+    d = dims_of(w)
+    say(f"fused evict with {distinct} distinct keys {d}")
+    _check(w, x, d, seed_note=f"{distinct} distinct: ")
