@@ -281,7 +281,7 @@ bkv_status evict_enqueue(const bkv_dims* d, int32_t flags, void* K, void* V, con
     char* w = static_cast<char*>(ws);
     float* sc = scores ? scores : reinterpret_cast<float*>(w + L.scores);
     int32_t* kp = kept ? kept : reinterpret_cast<int32_t*>(w + L.kept);
-    if (evict_fusable(L))
+    if (evict_fusable(*d, L))
         return map_hip(launch_evict_fused(*d, L, flags, K, V, q_win, beacons, counts, rope_cos, rope_sin, scale, sc,
                                           row_lse, kp, ws, stream));
     hipError_t e =

@@ -99,9 +99,11 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
                         void* ws, hipStream_t s);
 
 // The whole eviction in one launch (score, select and compact work items
-// under one per-head ticket); only where evict_fusable(L) (the bf16 fast
-// path).  kept and scores are required (the workspace's own may be passed).
-bool evict_fusable(const WsLayout& L);
+// under one per-head ticket); only where evict_fusable (the bf16 fast path,
+// heads of 16K to 32K tokens, where it measured at least as fast as the
+// chained launches).  kept and scores are required (the workspace's own may
+// be passed).
+bool evict_fusable(const bkv_dims& d, const WsLayout& L);
 hipError_t launch_evict_fused(const bkv_dims& d, const WsLayout& L, int flags, void* K, void* V, const void* q_win,
                               const float* beacons, const int32_t* counts, const float* rope_cos,
                               const float* rope_sin, float scale, float* scores, float* row_lse, int32_t* kept,

@@ -10,7 +10,7 @@ Checks per case:
   * bkv_score -> bkv_topk -> bkv_compact on a copy give the same kept
     indices and the same K and V bit for bit.
 Cases cover ragged N, D = 64, the prefix, W = 0, N <= budget, rows in several
-register groups, the scoring options, and layers whose keys repeat a few
+register groups (also four, one per wave), the scoring options, and layers whose keys repeat a few
 rows only, so that scores tie in bulk (the selection's exact radix path and
 its tie ranking by index)."""
 import numpy as np
@@ -25,16 +25,21 @@ from paper_2609_04971_amd import synth
 pytestmark = pytest.mark.gpu
 
 W = synth.Workload
+# the fused launch serves bf16 heads of 16K to 32K tokens (the chained calls
+# take the others), so every case has N in that range
 CASES = {
-    "ragged": W("f1", B=2, Hq=8, Hkv=2, D=128, N=1001, W=8, C=4, budget=300, revisit_frac=0.1),
-    "prefix": W("f2", B=2, Hq=8, Hkv=2, D=128, N=3000, W=16, C=8, budget=700, n_prefix=5),
-    "d64-g7": W("f3", B=1, Hq=14, Hkv=2, D=64, N=2100, W=5, C=3, budget=512, n_centroids=3),
-    "no-window": W("f4", B=1, Hq=8, Hkv=2, D=128, N=1500, W=0, C=8, budget=200),
-    "n-below-budget": W("f5", B=1, Hq=4, Hkv=2, D=128, N=90, W=8, C=4, budget=100),
-    "n-equals-budget": W("f6", B=1, Hq=4, Hkv=2, D=128, N=256, W=8, C=4, budget=256),
-    "two-row-groups": W("f7", B=1, Hq=14, Hkv=2, D=128, N=2000, W=24, C=16, budget=300, n_centroids=16),
-    "many-heads": W("f8", B=16, Hq=32, Hkv=8, D=128, N=8192, W=32, C=16, budget=1024, revisit_frac=0.05),
-    "long-64k": W("f9", B=1, Hq=8, Hkv=2, D=128, N=65536, W=128, C=32, budget=8192, revisit_frac=0.02),
+    "ragged": W("f1", B=2, Hq=8, Hkv=2, D=128, N=20001, W=8, C=4, budget=3000, revisit_frac=0.1),
+    "prefix": W("f2", B=2, Hq=8, Hkv=2, D=128, N=16384, W=16, C=8, budget=2000, n_prefix=5),
+    "d64-g7": W("f3", B=1, Hq=14, Hkv=2, D=64, N=17000, W=5, C=3, budget=2048, n_centroids=3),
+    "no-window": W("f4", B=1, Hq=8, Hkv=2, D=128, N=16500, W=0, C=8, budget=1000),
+    "n-below-budget": W("f5", B=1, Hq=4, Hkv=2, D=128, N=16384, W=8, C=4, budget=20000),
+    "n-equals-budget": W("f6", B=1, Hq=4, Hkv=2, D=128, N=16384, W=8, C=4, budget=16384),
+    "two-row-groups": W("f7", B=1, Hq=14, Hkv=2, D=128, N=16384, W=24, C=16, budget=1500, n_centroids=16),
+    "many-heads": W("f8", B=16, Hq=32, Hkv=8, D=128, N=16384, W=32, C=16, budget=2048, revisit_frac=0.05),
+    "32k": W("f9", B=1, Hq=8, Hkv=2, D=128, N=32768, W=32, C=16, budget=4096, revisit_frac=0.05),
+    # four row groups, one per wave (R = 16 + 7*64 = 464; D = 64: R = 16 + 4*107 = 444)
+    "four-row-groups": W("f11", B=1, Hq=14, Hkv=2, D=128, N=16900, W=64, C=16, budget=2048, n_centroids=16),
+    "four-row-groups-d64": W("f12", B=1, Hq=8, Hkv=2, D=64, N=16461, W=107, C=16, budget=1900, n_centroids=8),
 }
 
 
@@ -94,8 +99,9 @@ def test_fused_evict(name):
 
 
 @pytest.mark.parametrize("mean,causal", [(True, False), (False, True), (True, True)])
-def test_fused_evict_options(mean, causal):
-    w = CASES["prefix"]
+@pytest.mark.parametrize("name", ["prefix", "four-row-groups"])
+def test_fused_evict_options(name, mean, causal):
+    w = CASES[name]
     x = synth.make_layer(w, seed=72, device="cpu")
     d = dims_of(w)
     say(f"fused evict mean={mean} causal={causal} {d}")
@@ -107,7 +113,7 @@ def test_fused_evict_bulk_ties(distinct):
     # keys repeat `distinct` rows only: scores tie in bulk, so the threshold
     # value is shared by many candidates (one distinct row: every candidate
     # ties) and the kept ones among equals must be the lowest indices
-    w = W("f10", B=2, Hq=8, Hkv=2, D=128, N=4100, W=16, C=4, budget=900, n_prefix=2)
+    w = W("f10", B=2, Hq=8, Hkv=2, D=128, N=16500, W=16, C=4, budget=2100, n_prefix=2)
     x = synth.make_layer(w, seed=73, device="cpu")
     g = torch.Generator().manual_seed(74)
     pick = torch.randint(0, distinct, (w.B, w.Hkv, w.N), generator=g)
