@@ -838,13 +838,34 @@ __device__ __forceinline__ void stats_group(const uint16_t* st, int kb, const in
 }
 
 // The same statistics with each lane's offset fixed: after an item's first
-// group every lane holds a finite offset ms per row tile (its running max,
-// or 0 where it has seen no key), and later groups only add exp2(y - ms).
-// A later key more than 127 (log2 units) above the offset overflows the sum
-// to +inf; the item then redoes its statistics with the running max.  The
-// offset is a key the lane has seen, so the sum is at least 1 and no key
-// that matters underflows.  Two VALU instructions and one exp2 per (row,
-// key) instead of about four and a bit.
+// group every lane holds a finite offset per row tile (fix_offsets), and
+// later groups only add exp2(y - offset).  A later key more than 127 (log2
+// units) above the offset overflows the sum to +inf; the item then redoes
+// its statistics with the running max.  Two VALU instructions and one exp2
+// per (row, key) instead of about four and a bit.
+// Offsets of the fixed-offset statistics, taken after an item's first
+// group: per row, the largest logit (log2 units) any of the row's four lanes
+// has seen in that group, plus a margin of 64, or 0 for a row that has seen
+// no key; each lane's sum so far is rescaled to it.  The margin lets later
+// keys lie up to 191 above the first group's maximum before a sum overflows
+// (keys far above the first ones are common where queries revisit a few
+// keys); it costs nothing in precision: the sums stay above 2^-64, and a term
+// that flushes to zero lies more than 62 below the row's maximum.
+constexpr float kOffsetMargin = 64.f;
+
+template <int RT>
+__device__ __forceinline__ void fix_offsets(float* m, float* z, float* nms) {
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+        float mr = fmaxf(m[i], dev::shfl_xor_f(m[i], 16));
+        mr = fmaxf(mr, dev::shfl_xor_f(mr, 32));
+        const float off = (mr == -INFINITY) ? 0.f : mr + kOffsetMargin;
+        z[i] *= fast_exp2(m[i] - off);  // m = -inf: the sum is 0 and stays 0
+        m[i] = off;
+        nms[i] = -off;
+    }
+}
+
 template <int D, int RT, bool TAIL>
 __device__ __forceinline__ void stats_group_fixed(const uint16_t* st, int kb, const int* lim,
                                                   const Op<uint16_t, D>* yr, float s2, const float* nms, float* z,
@@ -1140,11 +1161,7 @@ __device__ __forceinline__ void fast_stats(const Args& a, int h, int chunk, Fast
             wait_group<D>(kg + 1 < ngroups);
             if (kg == 0) {
                 running_body(stA, kb);
-#pragma unroll
-                for (int i = 0; i < RT; ++i) {
-                    m[i] = (m[i] == -INFINITY) ? 0.f : m[i];
-                    nms[i] = -m[i];
-                }
+                fix_offsets<RT>(m, z, nms);
             } else {
                 fixed_body(stA, kb);
             }
@@ -1367,11 +1384,7 @@ __device__ void split_stats(const Args& a, int h, int chunk, FastSmem& sm, Stage
             if (kb >= N) break;
             if (sidx == 0 && q == 0) {  // the first group fixes each lane's offset
                 running_body(st.k[q], kb);
-#pragma unroll
-                for (int i = 0; i < RT; ++i) {
-                    m[i] = (m[i] == -INFINITY) ? 0.f : m[i];
-                    nms[i] = -m[i];
-                }
+                fix_offsets<RT>(m, z, nms);
             } else {
                 fixed_body(st.k[q], kb);
             }
