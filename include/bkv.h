@@ -172,7 +172,11 @@ bkv_status bkv_score_ex(const bkv_dims* d, int32_t flags, const void* K, const v
  * ties to the lower index (-0 equals +0); kept is emitted in ascending
  * order (Section 2.2 TopK; Algorithm 2, the I_keep, k_sel, TopK and Sort
  * steps).  scores [B,Hkv,N] read; kept [B,Hkv,min(budget,N)] written.
- * Needs no workspace (ws may be NULL). */
+ * ws is optional (NULL: one workgroup per head).  With a workspace of at
+ * least bkv_workspace_bytes(d, BKV_OP_TOPK) bytes (0 when the dims never
+ * split), initialised by bkv_workspace_init, a layer of few heads of more
+ * than 8192 tokens splits each head over several workgroups (three kernel
+ * launches); the result is the same. */
 bkv_status bkv_topk(const bkv_dims* d, const float* scores, int32_t* kept, void* ws,
                     size_t ws_bytes, hipStream_t stream);
 

@@ -46,6 +46,16 @@ WsLayout ws_layout(const bkv_dims& d) {
     off = align_up(off + sizeof(int) * (size_t)P * kHcWords);
     L.cflags = off;
     off = align_up(off + sizeof(int) * (size_t)P * L.nseg);
+    if (d.N > d.budget && d.N > kTkMinN && P <= kTkMaxHeads) {  // heads may be split for selection
+        L.tk_hist = off;
+        off = align_up(off + sizeof(int) * (size_t)P * 4096);
+        L.tk_head = off;
+        off = align_up(off + sizeof(int) * (size_t)P * kTkHeadWords);
+        L.tk_cand = off;
+        off = align_up(off + sizeof(uint32_t) * 2 * (size_t)P * 512);
+        L.tk_cnt = off;
+        off = align_up(off + sizeof(int) * (size_t)P * kTkMaxSlices);
+    }
     L.ctl_end = off;
     // data (depends on N, W, C as well)
     const int R = d.C + G * d.W;
@@ -127,6 +137,7 @@ size_t bkv_workspace_bytes(const bkv_dims* d, int32_t op) {
     const WsLayout L = ws_layout(*d);
     switch (op) {
         case BKV_OP_SCORE: return L.score_end;
+        case BKV_OP_TOPK: return L.tk_hist ? L.ctl_end : 0;
         case BKV_OP_COMPACT: return L.ctl_end;
         case BKV_OP_EVICT: return L.evict_end;
         default: return 0;
@@ -202,13 +213,15 @@ bkv_status bkv_score_ex(const bkv_dims* d, int32_t flags, const void* K, const v
 
 bkv_status bkv_topk(const bkv_dims* d, const float* scores, int32_t* kept, void* ws, size_t ws_bytes,
                     hipStream_t stream) {
-    (void)ws;
-    (void)ws_bytes;
     bkv_status st = bkv_validate(d, BKV_OP_TOPK);
     if (st != BKV_OK) return st;
     if (empty_batch(d) || d->N == 0) return BKV_OK;
     if (!scores || !kept) return BKV_ERR_INVALID;
-    return map_hip(launch_topk(*d, scores, kept, stream));
+    const WsLayout L = ws_layout(*d);
+    // the split selection needs the workspace's control block; without it
+    // (or with a smaller buffer) every head takes one workgroup
+    void* w = (ws && L.tk_hist && ws_bytes >= L.ctl_end) ? ws : nullptr;
+    return map_hip(launch_topk(*d, L, scores, kept, w, stream));
 }
 
 bkv_status bkv_compact(const bkv_dims* d, void* K, void* V, const int32_t* kept, void* ws, size_t ws_bytes,
@@ -287,7 +300,7 @@ bkv_status evict_enqueue(const bkv_dims* d, int32_t flags, void* K, void* V, con
     hipError_t e =
         launch_score(*d, L, flags, K, q_win, beacons, counts, rope_cos, rope_sin, scale, sc, row_lse, ws, stream);
     if (e != hipSuccess) return BKV_ERR_HIP;
-    e = launch_topk(*d, sc, kp, stream);
+    e = launch_topk(*d, L, sc, kp, ws, stream);
     if (e != hipSuccess) return BKV_ERR_HIP;
     return map_hip(launch_compact(*d, L, K, V, kp, ws, stream));
 }

@@ -57,6 +57,11 @@ struct WsLayout {
     // control block
     size_t hctl;    // per-head control lines (int32 [P][kHcWords])
     size_t cflags;  // compaction: per-segment read-done flags (int32 [P][nseg])
+    // selection split over several workgroups per head (0: not laid out)
+    size_t tk_hist;  // int32 [P][4096] bin counts, left zero after each selection
+    size_t tk_head;  // int32 [P][kTkHeadWords]
+    size_t tk_cand;  // uint32 [P][512][2] threshold-bin (order key, token)
+    size_t tk_cnt;   // int32 [P][kTkMaxSlices] per-slice counts
     size_t ctl_end;
     // data
     size_t part_m, part_z;  // score: per-chunk row statistics (fp32 [P][nch][R_pad_max])
@@ -74,6 +79,13 @@ struct WsLayout {
 // The score fast path (bf16) holds the rows of one row group in registers:
 // at most kFastTiles tiles per group and kFastRowGroups groups.
 constexpr int kFastTiles = 9;
+
+// Split selection: words per head, slices per head at most, heads at most
+// for which the regions are laid out, and the shortest head it takes.
+constexpr int kTkHeadWords = 4;
+constexpr int kTkMaxSlices = 64;
+constexpr int kTkMaxHeads = 128;
+constexpr int kTkMinN = 8192;
 constexpr int kFastRowGroups = 8;
 
 WsLayout ws_layout(const bkv_dims& d);
@@ -109,7 +121,11 @@ hipError_t launch_evict_fused(const bkv_dims& d, const WsLayout& L, int flags, v
                               const float* rope_sin, float scale, float* scores, float* row_lse, int32_t* kept,
                               void* ws, hipStream_t s);
 
-hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hipStream_t s);
+// Selection; with a workspace holding the split-selection regions (ws
+// non-null, L.tk_hist set) a layer of few heads is split over several
+// workgroups per head.
+hipError_t launch_topk(const bkv_dims& d, const WsLayout& L, const float* scores, int32_t* kept, void* ws,
+                       hipStream_t s);
 hipError_t launch_compact_fill(const bkv_dims& d, void* K, void* V, const int32_t* kept, int32_t* src_of, void* ws,
                                hipStream_t s);
 

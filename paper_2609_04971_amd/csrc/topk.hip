@@ -144,7 +144,7 @@ struct GlobalKeys {
 
 template <class Keys>
 __device__ void topk_head(const float* __restrict__ scores, int32_t* __restrict__ kept, int N, int budget, int W,
-                          int n_prefix, int n_keep, Keys& keys) {
+                          int n_prefix, int n_keep, Keys& keys, int h) {
     __shared__ int hist[kWaves][256];  // also the kBins value histogram
     static_assert(kWaves * 256 == kBins, "LDS reuse");
     __shared__ int tot[256];
@@ -155,7 +155,6 @@ __device__ void topk_head(const float* __restrict__ scores, int32_t* __restrict_
     __shared__ int s_digit, s_above, s_ncand, s_need;
     __shared__ uint32_t s_theta;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int h = blockIdx.x;
     int32_t* out = kept + (size_t)h * n_keep;
 
     if (N <= budget) {
@@ -324,7 +323,7 @@ __device__ void topk_head(const float* __restrict__ scores, int32_t* __restrict_
 __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict__ scores, int32_t* __restrict__ kept,
                                                          int N, int budget, int W, int n_prefix, int n_keep) {
     GlobalKeys keys;
-    topk_head(scores, kept, N, budget, W, n_prefix, n_keep, keys);
+    topk_head(scores, kept, N, budget, W, n_prefix, n_keep, keys, blockIdx.x);
 }
 
 // Suffix scan over the 256 digit counts tot[] by wave 0: the digit d at
@@ -639,11 +638,299 @@ __global__ __launch_bounds__(kThreads) void topk_reg_kernel(const float* __restr
     }
 }
 
+
+// ---- heads split over several workgroups ------------------------------------
+//
+// A layer of fewer heads than twice the compute units leaves most of the
+// machine idle with one workgroup per head, so each head's tokens are cut
+// into M slices of at most kSliceMax, one workgroup each, over three
+// launches (the kernel boundaries are the only synchronisation):
+//   hist: each slice bins its candidates' scores over the fixed range
+//         [-32, 0) nats (kBins bins; scores at or above 0 and NaN go to the
+//         top bin, scores below -32 to the bottom one) and adds its counts
+//         to the head's histogram in the workspace;
+//   cut:  every slice finds the threshold bin T of the head from the full
+//         histogram, counts its candidates above T, and lists those in T
+//         (order key, token) in the workspace;
+//   emit: every slice ranks the threshold bin's list by (key descending,
+//         token ascending), which decides each listed token exactly; its
+//         output position is the number of kept tokens in lower slices (the
+//         forced ones, the counts above T and the listed kept tokens below
+//         it) plus its rank within the slice.
+// Scores returned by bkv_score are log-weights at or below 0, so the
+// threshold bin rarely holds more than a few dozen tokens.  A head whose
+// threshold bin lists more than kMaxRank tokens (ties in bulk, or a
+// threshold far outside the range), or a workspace without the library's
+// stamp, is selected whole by one workgroup of the emit launch with the
+// one-workgroup algorithm above.
+constexpr int kSliceMax = 16384;
+constexpr int kSlicePer = kSliceMax / kThreads;  // tokens per thread at most
+constexpr float kFixLo = -32.f;
+constexpr float kFixScale = kBins / 32.f;  // bins per nat
+
+// Bin of order key u over the fixed range: monotone non-decreasing in the key.
+__device__ __forceinline__ int fixed_bin(uint32_t u) {
+    if (u >= 0x80000000u) return kBins - 1;  // +0, positive scores, +inf, NaN
+    const float v = key_to_float(u);          // negative scores and -inf (-NaN: NaN, to bin 0)
+    return (int)fminf(fmaxf(floorf((v - kFixLo) * kFixScale), 0.f), (float)(kBins - 1));
+}
+
+struct SplitArgs {
+    const float* scores;
+    int32_t* kept;
+    int N, budget, W, n_prefix, n_keep, P, M, slice;
+    const int* hdr;  // workspace header (stamp)
+    int* hist;       // [P][kBins] counts of the candidates' bins (left zero by the emit)
+    int* head;       // [P][kTkHeadWords]: listed tokens, threshold bin, count above it
+    uint32_t* cand;  // [P][kMaxRank][2]: the threshold bin's (order key, token)
+    int* acnt;       // [P][kTkMaxSlices]: candidates above the threshold bin per slice
+};
+
+__device__ __forceinline__ int tk_ksel(const SplitArgs& a) { return a.budget - a.n_prefix - a.W; }
+
+__global__ __launch_bounds__(kThreads) void topk_hist_kernel(SplitArgs a) {
+    __shared__ int lh[kBins];
+    const int h = blockIdx.x / a.M, sl = blockIdx.x % a.M, tid = threadIdx.x;
+    if (sl == 0 && tid == 0) a.head[h * kTkHeadWords] = 0;  // the list of the cut launch starts empty
+    if (tk_ksel(a) <= 0) return;
+    const int lo = max(a.n_prefix, sl * a.slice), hi = min(a.N - a.W, (sl + 1) * a.slice);
+    for (int i = tid; i < kBins; i += kThreads) lh[i] = 0;
+    __syncthreads();
+    const float* row = a.scores + (size_t)h * a.N;
+    float v[kSlicePer];
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i) {
+        const int j = lo + tid + i * kThreads;
+        v[i] = j < hi ? row[j] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i)
+        if (lo + tid + i * kThreads < hi) atomicAdd(&lh[fixed_bin(order_key(v[i]))], 1);
+    __syncthreads();
+    int* gh = a.hist + (size_t)h * kBins;
+    for (int i = tid; i < kBins; i += kThreads) {
+        const int c = lh[i];
+        if (c) atomicAdd(&gh[i], c);
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void topk_cut_kernel(SplitArgs a) {
+    __shared__ int scan_buf[kWaves + 1];
+    __shared__ int s_digit, s_above;
+    const int h = blockIdx.x / a.M, sl = blockIdx.x % a.M, tid = threadIdx.x;
+    const int ksel = tk_ksel(a);
+    if (ksel <= 0) return;
+    // this slice's candidates in flight while the histogram is read
+    const int lo = max(a.n_prefix, sl * a.slice), hi = min(a.N - a.W, (sl + 1) * a.slice);
+    const float* row = a.scores + (size_t)h * a.N;
+    float v[kSlicePer];
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i) {
+        const int j = lo + tid + i * kThreads;
+        v[i] = j < hi ? row[j] : 0.f;
+    }
+    // the bin holding the ksel-th candidate from the top (every slice finds
+    // the same one; the candidates outnumber ksel since N > budget)
+    if (tid == 0) {
+        s_digit = 0;
+        s_above = 0;
+    }
+    __syncthreads();
+    find_wide_digit(a.hist + (size_t)h * kBins, ksel, scan_buf, &s_digit, &s_above);
+    __syncthreads();
+    const int T = s_digit;
+    int* hw = a.head + h * kTkHeadWords;
+    if (sl == 0 && tid == 0) {
+        hw[1] = T;
+        hw[2] = s_above;
+    }
+    uint32_t* ch = a.cand + (size_t)h * kMaxRank * 2;
+    int above = 0;
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i) {
+        const int j = lo + tid + i * kThreads;
+        if (j >= hi) break;
+        const uint32_t u = order_key(v[i]);
+        const int b = fixed_bin(u);
+        above += b > T;
+        if (b == T) {
+            const int p = atomicAdd(&hw[0], 1);
+            if (p < kMaxRank) {
+                ch[2 * p] = u;
+                ch[2 * p + 1] = (uint32_t)j;
+            }
+        }
+    }
+    int total;
+    block_excl_scan(above, scan_buf, &total);
+    if (tid == 0) a.acnt[h * kTkMaxSlices + sl] = total;
+}
+
+__global__ __launch_bounds__(kThreads) void topk_emit_kernel(SplitArgs a) {
+    __shared__ uint32_t ck[kMaxRank];
+    __shared__ int ci[kMaxRank];
+    __shared__ uint32_t tbits[kSliceMax / 32];  // listed tokens of this slice that are kept
+    __shared__ int runs[kSlicePer * kWaves];
+    __shared__ int scan_buf[kWaves + 1];
+    __shared__ int s_below, s_lower;
+    const int h = blockIdx.x / a.M, sl = blockIdx.x % a.M, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int N = a.N, ksel = tk_ksel(a);
+    const int* hw = a.head + h * kTkHeadWords;
+    // every independent load in flight at once: the head's words, the stamp,
+    // the counts of lower slices and this slice's scores
+    const int j0 = sl * a.slice, j1 = min(N, j0 + a.slice);
+    const float* row = a.scores + (size_t)h * N;
+    float v[kSlicePer];
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i) {
+        const int j = j0 + tid + i * kThreads;
+        v[i] = j < j1 ? row[j] : 0.f;
+    }
+    const int hw0 = hw[0], hw1 = hw[1], hw2 = hw[2];
+    const int lower = (ksel > 0 && tid < sl) ? a.acnt[h * kTkMaxSlices + tid] : 0;  // sl < 64
+    const int n = ksel > 0 ? hw0 : 0;
+    const bool stamped = (uint32_t)a.hdr[kHdrMagic] == kWsMagic && a.hdr[kHdrP] == a.P;
+    {   // this slice's share of the head's histogram is cleared for the next call
+        int* gh = a.hist + (size_t)h * kBins;
+        for (int i = sl * kBins / a.M + tid; i < (sl + 1) * kBins / a.M; i += kThreads) gh[i] = 0;
+    }
+    if (!stamped || n > kMaxRank) {
+        if (sl == 0) {
+            GlobalKeys keys;
+            topk_head(a.scores, a.kept, N, a.budget, a.W, a.n_prefix, a.n_keep, keys, h);
+        }
+        return;
+    }
+    const int T = ksel > 0 ? hw1 : kBins;
+    const int rem = ksel > 0 ? ksel - hw2 : 0;  // listed tokens to keep
+    const uint32_t* ch = a.cand + (size_t)h * kMaxRank * 2;
+    for (int i = tid; i < n; i += kThreads) {
+        ck[i] = ch[2 * i];
+        ci[i] = (int)ch[2 * i + 1];
+    }
+    for (int i = tid; i < kSliceMax / 32; i += kThreads) tbits[i] = 0u;
+    if (tid == 0) s_below = 0;
+    int lower_sum = lower;  // wave 0 holds the lower slices' counts (sl < 64)
+    if (tid < 64) {
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) lower_sum += __shfl_xor(lower_sum, o, 64);
+        if (tid == 0) s_lower = lower_sum;
+    }
+    __syncthreads();
+    if (tid < n) {
+        const uint32_t mk = ck[tid];
+        const int mi = ci[tid];
+        int rank = 0;
+        for (int c = 0; c < n; ++c) rank += (ck[c] > mk) || (ck[c] == mk && ci[c] < mi);
+        if (rank < rem) {
+            if (mi < j0)
+                atomicAdd(&s_below, 1);
+            else if (mi < j1)
+                atomicOr(&tbits[(mi - j0) >> 5], 1u << ((mi - j0) & 31));
+        }
+    }
+    __syncthreads();
+    // kept tokens before this slice: forced ones, those above T, listed ones
+    const int lo = a.n_prefix, hi = N - a.W;  // candidates [lo, hi)
+    const int base = min(j0, lo) + max(0, j0 - hi) + s_below + s_lower;
+    // token j0 + tid + i * kThreads (coalesced); runs of 64 tokens in order
+    const int per = (j1 - j0 + kThreads - 1) / kThreads;
+    uint32_t keep = 0;
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i) {
+        if (i >= per) break;
+        const int j = j0 + tid + i * kThreads;
+        bool k = false;
+        if (j < j1) {
+            if (j < lo || j >= hi) {
+                k = true;
+            } else if (ksel > 0) {
+                const int b = fixed_bin(order_key(v[i]));
+                k = b > T || (b == T && ((tbits[(j - j0) >> 5] >> ((j - j0) & 31)) & 1u));
+            }
+        }
+        keep |= (k ? 1u : 0u) << i;
+        const uint64_t kb = __builtin_amdgcn_ballot_w64(k);
+        if (lane == 0) runs[i * kWaves + wave] = (int)__builtin_popcountll(kb);
+    }
+    __syncthreads();
+    {
+        const int nr = per * kWaves;
+        const int v = tid < nr ? runs[tid] : 0;
+        int total;
+        const int before = block_excl_scan(v, scan_buf, &total);
+        if (tid < nr) runs[tid] = before;
+        __syncthreads();
+    }
+    int32_t* out = a.kept + (size_t)h * a.n_keep;
+#pragma unroll
+    for (int i = 0; i < kSlicePer; ++i) {
+        if (i >= per) break;
+        const bool k = (keep >> i) & 1u;
+        const uint64_t kb = __builtin_amdgcn_ballot_w64(k);
+        if (k) {
+            const int pos = base + runs[i * kWaves + wave] + rank_in_wave(kb);
+            if (pos < a.n_keep) out[pos] = j0 + tid + i * kThreads;
+        }
+    }
+}
+
 }  // namespace
 
-hipError_t launch_topk(const bkv_dims& d, const float* scores, int32_t* kept, hipStream_t s) {
+// Slices per head of the split selection for this layer on this device;
+// 1: one workgroup per head.
+int topk_slices(const bkv_dims& d, int* slice) {
+    const int P = d.B * d.Hkv;
+    if (d.N <= d.budget || d.N <= kTkMinN || P < 1) return 1;
+    int dev_id = 0, cus = 256;
+    if (hipGetDevice(&dev_id) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev_id) != hipSuccess)
+        cus = 256;
+    // about two workgroups per compute unit; split only where a head would
+    // otherwise leave seven of eight compute units idle (measured: 32 heads
+    // of 64K tokens 109 -> 33 us, of 16K 20 -> 19 us; 128 heads of 32K
+    // 23 us with one workgroup each, 32 us split)
+    const int m0 = (2 * cus + P - 1) / P;
+    if (m0 < 8) return 1;
+    int sl = (d.N + m0 - 1) / m0;
+    sl = (sl + 63) / 64 * 64;
+    if (sl < 2048) sl = 2048;
+    if (sl > kSliceMax) sl = kSliceMax;
+    const int M = (d.N + sl - 1) / sl;
+    if (M < 2 || M > kTkMaxSlices) return 1;
+    *slice = sl;
+    return M;
+}
+
+hipError_t launch_topk(const bkv_dims& d, const WsLayout& L, const float* scores, int32_t* kept, void* ws,
+                       hipStream_t s) {
     const int P = d.B * d.Hkv;
     const int n_keep = d.N < d.budget ? d.N : d.budget;
+    int slice = 0;
+    const int M = (ws && L.tk_hist && P <= kTkMaxHeads) ? topk_slices(d, &slice) : 1;
+    if (M > 1) {
+        char* w = static_cast<char*>(ws);
+        SplitArgs a;
+        a.scores = scores;
+        a.kept = kept;
+        a.N = d.N;
+        a.budget = d.budget;
+        a.W = d.W;
+        a.n_prefix = d.n_prefix;
+        a.n_keep = n_keep;
+        a.P = P;
+        a.M = M;
+        a.slice = slice;
+        a.hdr = reinterpret_cast<const int*>(w);
+        a.hist = reinterpret_cast<int*>(w + L.tk_hist);
+        a.head = reinterpret_cast<int*>(w + L.tk_head);
+        a.cand = reinterpret_cast<uint32_t*>(w + L.tk_cand);
+        a.acnt = reinterpret_cast<int*>(w + L.tk_cnt);
+        hipLaunchKernelGGL(topk_hist_kernel, dim3(P * M), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(topk_cut_kernel, dim3(P * M), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(topk_emit_kernel, dim3(P * M), dim3(kThreads), 0, s, a);
+        return hipGetLastError();
+    }
     if (d.N <= 8 * kThreads)
         hipLaunchKernelGGL(topk_reg_kernel<8>, dim3(P), dim3(kThreads), 0, s, scores, kept, d.N, d.budget, d.W,
                            d.n_prefix, n_keep);

@@ -19,6 +19,10 @@ CASES = {
     "gqa7-d64": (W("e2", B=1, Hq=28, Hkv=4, D=64, N=2100, W=9, C=16, budget=512, n_centroids=16, zipf=1.2), 0),
     "n-below-budget": (W("e3", B=1, Hq=4, Hkv=2, D=128, N=90, W=8, C=4, budget=100), 0),
     "only-forced": (W("e4", B=1, Hq=4, Hkv=2, D=128, N=900, W=60, C=4, budget=64), 4),
+    # chained calls with the selection split over several workgroups per head:
+    # an fp32 layer (generic score path) and a bf16 head past 32K tokens
+    "split-select-fp32": (W("e5", B=1, Hq=8, Hkv=2, D=64, N=12000, W=16, C=4, budget=1500, dtype="fp32"), 2),
+    "split-select-40k": (W("e6", B=1, Hq=8, Hkv=2, D=128, N=40000, W=32, C=8, budget=5000, revisit_frac=0.05), 0),
 }
 
 

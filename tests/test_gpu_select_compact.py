@@ -32,6 +32,14 @@ def _scores(P, N, seed, kind):
     elif kind == "minus-inf":
         s = -torch.rand(P, N, generator=g)
         s[:, ::3] = float("-inf")
+    elif kind == "plus-inf":  # a few +inf: kept whatever the threshold
+        s = -torch.rand(P, N, generator=g) * 12
+        s[:, 7::97] = float("inf")
+    elif kind == "far":  # every score far below the split selection's bin range
+        s = -1000.0 - torch.rand(P, N, generator=g) * 100
+    elif kind == "mixed":  # heads alternate between spread scores and one value
+        s = -torch.rand(P, N, generator=g) * 12
+        s[1::2] = -2.5
     return s.contiguous()
 
 
@@ -56,17 +64,61 @@ TOPK = [
 ]
 
 
-@pytest.mark.parametrize("case", TOPK, ids=[f"{c[6]}-N{c[2]}-b{c[3]}" for c in TOPK])
-def test_topk_bit_exact(case):
+# heads split over several workgroups (a workspace given, few heads, N > 8192)
+TOPK_SPLIT = [
+    (1, 2, 20000, 3000, 16, 3, "normal"),     # ragged last slice
+    (1, 2, 9000, 100, 20, 5, "normal"),       # just past the shortest split head
+    (1, 2, 20000, 20, 12, 8, "normal"),       # k_sel == 0
+    (2, 2, 20000, 2000, 8, 0, "equal"),       # every head ties in bulk: one workgroup selects it
+    (2, 2, 20000, 2000, 8, 0, "mixed"),       # split heads beside whole-head ones
+    (1, 2, 20000, 2000, 8, 0, "wide"),        # half the scores above the range
+    (1, 2, 20000, 2000, 8, 0, "far"),         # all below the range
+    (1, 2, 20000, 2000, 8, 0, "plus-inf"),
+    (1, 2, 20000, 2000, 8, 0, "cluster300"),  # hundreds of candidates in the threshold bin
+    (2, 2, 32768, 4096, 32, 2, "ties"),
+    (4, 8, 65536, 8192, 128, 0, "normal"),    # the 64K layer's shape (32 heads of 16 slices)
+]
+
+
+def _topk_ws(d, split):
+    if not split or bkv.workspace_bytes(d, bkv.OP_TOPK) == 0:
+        return None
+    return bkv.workspace(d, bkv.OP_TOPK)
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["one-wg", "ws"])
+@pytest.mark.parametrize("case", TOPK + TOPK_SPLIT, ids=[f"{c[6]}-B{c[0]}H{c[1]}-N{c[2]}-b{c[3]}" for c in TOPK + TOPK_SPLIT])
+def test_topk_bit_exact(case, split):
     B, Hkv, N, budget, W, n_prefix, kind = case
     d = bkv.dims(B=B, Hq=Hkv, Hkv=Hkv, D=128, N=N, W=W, C=1, budget=budget, n_prefix=n_prefix)
     s = _scores(B * Hkv, N, seed=N + budget, kind=kind).view(B, Hkv, N)
-    say(f"topk {case}")
+    ws = _topk_ws(d, split)
+    say(f"topk {case} workspace={ws is not None}")
     kept = torch.full((B, Hkv, d.n_keep), -1, dtype=torch.int32, device="cuda")
-    bkv.topk(d, s.cuda(), kept)
+    bkv.topk(d, s.cuda(), kept, ws)
     got = host(kept).numpy()
     want = oracle.topk(s.double().numpy(), budget, W, n_prefix)
     np.testing.assert_array_equal(got, want)
+
+
+def test_topk_split_calls_in_a_row_and_unstamped_workspace():
+    # the split selection leaves its histogram clear for the next call on the
+    # same workspace; a workspace without the stamp falls back to one
+    # workgroup per head and stays exact
+    d = bkv.dims(B=2, Hq=2, Hkv=2, D=128, N=30000, W=16, C=1, budget=3000, n_prefix=1)
+    ws = bkv.workspace(d, bkv.OP_TOPK)
+    assert ws.numel() >= bkv.workspace_bytes(d, bkv.OP_TOPK) > 0
+    for seed, kind in [(1, "normal"), (2, "cluster200"), (3, "normal")]:
+        s = _scores(4, d.N, seed=seed, kind=kind).view(2, 2, d.N)
+        kept = torch.full((2, 2, d.n_keep), -1, dtype=torch.int32, device="cuda")
+        say(f"topk split, call with seed {seed}")
+        bkv.topk(d, s.cuda(), kept, ws)
+        np.testing.assert_array_equal(host(kept).numpy(), oracle.topk(s.double().numpy(), d.budget, d.W, 1))
+    raw = torch.zeros_like(ws)
+    s = _scores(4, d.N, seed=9, kind="normal").view(2, 2, d.N)
+    kept = torch.full((2, 2, d.n_keep), -1, dtype=torch.int32, device="cuda")
+    bkv.topk(d, s.cuda(), kept, raw)
+    np.testing.assert_array_equal(host(kept).numpy(), oracle.topk(s.double().numpy(), d.budget, d.W, 1))
 
 
 def _kv(P, Ncap, D, dtype, seed):
