@@ -7,35 +7,44 @@
 // softmax attention normalised over all N keys (Eq. 4), aggregated by max
 // over every query and head of the group (Eq. 6, max form).
 //
-// One launch does it all.  Each head gets 2 * nch workgroups, which take a
-// per-head ticket when they start: the first nch tickets are
-//   S(h, c)  row statistics (running max m, sum z) of l over key chunk c;
-//            the last S item of a head folds them into lse_r;
+// One launch scores a layer.  Each head gets 2 * nch workgroups, which
+// take a per-head ticket when they start: the first nch tickets are
+//   S(h, c)  row statistics (max m, sum z) of l over key chunk c; the last
+//            S item of a head folds them into lse_r;
 // and the next nch are
 //   F(h, c)  recompute l for chunk c and write s_j = max_r (l_rj - lse_r).
 // An F item waits only for the S items of its head, which hold lower
 // tickets, have started, and never wait, so the schedule cannot deadlock
-// whatever the residency.  The grid lists a head's workgroups `lag` heads
-// after the head's first ones, so the second read of a head's keys follows
+// whatever the residency.  The grid lists a head's F workgroups `lag`
+// heads after its S workgroups, so the second read of a head's keys follows
 // the first closely (it tends to hit the MI355X's memory-side cache rather
-// than HBM).
+// than HBM).  The fused eviction (evict_kernel, below) adds a selection and
+// compaction items per head under the same tickets.
 //
-// Every item builds its own observation rows in LDS from the read-only
-// inputs (RoPE, then rounding to the cache dtype), so the only data passed
-// between work items are the per-chunk statistics and lse, a few KB per
-// head.  Those go through agent-scope atomic loads and stores, which are
-// coherent across the MI355X's per-XCD L2 caches by themselves; a producer
-// waits for its stores to complete (s_waitcnt) before the counter or flag
-// that publishes them, so no L2 write-back or invalidation is needed.
+// The only data passed between work items are the per-chunk statistics and
+// lse, a few KB per head.  Those go through agent-scope atomic loads and
+// stores, which are coherent across the MI355X's per-XCD L2 caches by
+// themselves; a producer waits for its stores to complete (s_waitcnt)
+// before the counter or flag that publishes them, so no L2 write-back or
+// invalidation is needed.
 //
 // Logits come from v_mfma_f32_16x16x32_bf16 (fp32 accumulation of exact
-// bf16 products; fp32 caches use v_mfma_f32_16x16x4_f32).  Key tiles are
-// read straight from HBM into MFMA operand registers with 16-byte loads (no
-// LDS staging), laid out so each load instruction covers 64 contiguous
-// bytes of each of 16 rows; the observation rows sit in LDS.  Statistics are kept in log2
-// units (v_exp_f32 computes 2^x): s2 = scale * log2(e).  In F items the
-// accumulator starts at -lse2_r / s2, so the MFMA yields l_rj - lse_r (up
-// to the factor s2) directly and the epilogue is one max per element.
+// bf16 products; fp32 caches use v_mfma_f32_16x16x4_f32).  Statistics are
+// kept in log2 units (v_exp_f32 computes 2^x): s2 = scale * log2(e).  In F
+// items the accumulator starts at -lse2_r / s2, so the MFMA yields
+// l_rj - lse_r (up to the factor s2) directly and the epilogue is one max
+// per element.  Two paths:
+//   fast (bf16, R <= 1152): a rows kernel first writes each head's
+//     observation rows to the workspace in MFMA operand order; work items
+//     hold a group of up to 144 rows in registers and stage 32-key groups
+//     of K through LDS (direct-to-LDS loads, double-buffered per wave).
+//     Heads of four row groups give each wave one group and share one key
+//     stream among the four waves (row split); see the sections below.
+//   generic (fp32, or more rows): every item builds its rows in LDS from
+//     the read-only inputs (RoPE, then rounding to the cache dtype) and
+//     reads key tiles straight from HBM into MFMA operand registers with
+//     16-byte loads, each load instruction covering 64 contiguous bytes of
+//     each of 16 rows.
 #include <math.h>
 #include <string.h>
 
