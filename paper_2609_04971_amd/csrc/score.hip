@@ -862,6 +862,23 @@ __device__ __forceinline__ void stats_group(const uint16_t* st, int kb, const in
 // that flushes to zero lies more than 62 below the row's maximum.
 constexpr float kOffsetMargin = 64.f;
 
+// A lane's statistics before they are merged: the sum's binary exponent
+// moves into the offset, so z lies in [0.5, 1) and m is within one of the
+// lane's log2-sum.  A sum taken against a fixed offset can be as large as
+// 2^127, and merges scale sums by exp2(m - M): without this, a chunk whose
+// offset lies more than 126 below another chunk's would lose its sum to a
+// factor that underflows, however large the sum.  A lane that saw no key
+// (z = 0) gets m = -inf.
+__device__ __forceinline__ void normalise_mz(float& m, float& z) {
+    if (z == 0.f) {
+        m = -INFINITY;
+        return;
+    }
+    int e;
+    z = frexpf(z, &e);
+    m += (float)e;
+}
+
 template <int RT>
 __device__ __forceinline__ void fix_offsets(float* m, float* z, float* nms) {
 #pragma unroll
@@ -1201,7 +1218,7 @@ __device__ __forceinline__ void fast_stats(const Args& a, int h, int chunk, Fast
             }
         }
 #pragma unroll
-        for (int i = 0; i < RT; ++i) m[i] = (z[i] == 0.f) ? -INFINITY : m[i];  // a lane that saw no key
+        for (int i = 0; i < RT; ++i) normalise_mz(m[i], z[i]);
         // lanes sharing a row: g = 0..3, then waves
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
@@ -1432,7 +1449,7 @@ __device__ void split_stats(const Args& a, int h, int chunk, FastSmem& sm, Stage
         }
     }
 #pragma unroll
-    for (int i = 0; i < RT; ++i) m[i] = (z[i] == 0.f) ? -INFINITY : m[i];
+    for (int i = 0; i < RT; ++i) normalise_mz(m[i], z[i]);
     // this wave's rows: lanes sharing a row (g = 0..3) meet, then go out
     const size_t pbase = ((size_t)h * a.nch + chunk) * a.R_pad_max + (size_t)wave * RT * 16;
 #pragma unroll

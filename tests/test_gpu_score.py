@@ -135,6 +135,41 @@ def test_score_deterministic():
 
 
 @pytest.mark.parametrize("mean", [False, True])
+def test_score_offsets_far_apart_between_chunks(mean):
+    # one recent row sees a key of ~104 nats in the first group of one work
+    # item and its largest key, ~131 nats, inside a later item whose first
+    # keys are ordinary: the items' offsets lie more than 126 (log2 units)
+    # apart while the later item's sum is far from overflow; merging their
+    # statistics must keep the later sum
+    import paper_2609_04971_amd as bkv
+    w = W("c10", B=2, Hq=8, Hkv=2, D=128, N=3000, W=8, C=4, budget=500)
+    x = synth.make_layer(w, seed=23, device="cpu")
+    K = x["K"].float()
+    for b in range(w.B):
+        for h in range(w.Hkv):
+            y = x["q_win"][b, h * w.G].float()[0]
+            for j, nats in ((256 + 3, 104.0), (1024 + 170, 131.0)):
+                K[b, h, j] = nats * np.sqrt(w.D) * y / y.norm() ** 2
+    x["K"] = K.to(torch.bfloat16).contiguous()
+    d = dims_of(w)
+    s_ref, lse_ref = oracle.score(x["K"], x["q_win"], x["beacons"], x["counts"], N=w.N, rope_cos=x["rope_cos"],
+                                  rope_sin=x["rope_sin"], threads=4, agg="mean" if mean else "max")
+    assert lse_ref[..., w.C].max() > 120.0, "the planted keys do not dominate their row"
+    xd = to_dev(x)
+    ws = bkv.workspace(d, bkv.OP_SCORE)
+    scores = torch.full((d.B, d.Hkv, d.N), float("nan"), device="cuda")
+    lse = torch.full((d.B, d.Hkv, d.C + d.G * d.W), float("nan"), device="cuda")
+    say(f"score with offsets far apart between items, mean={mean}: {d}")
+    bkv.score(d, xd["K"], xd["q_win"], xd["beacons"], xd["counts"], scores, ws, row_lse=lse,
+              rope_cos=xd["rope_cos"], rope_sin=xd["rope_sin"], mean=mean)
+    torch.cuda.synchronize()
+    assert bkv.device_status(ws) == bkv.OK
+    err = assert_scores_close(host(scores).numpy(), s_ref)
+    assert_scores_close(host(lse).numpy(), lse_ref, "row_lse")
+    say(f"  max |diff| {err:.2e}")
+
+
+@pytest.mark.parametrize("mean", [False, True])
 def test_score_key_far_above_its_lanes_first_keys(mean):
     # a key whose logit for a row lies ~300 nats above everything else: it is
     # not among the first keys a wave sees in its work item, so the row's

@@ -92,6 +92,32 @@ def test_split_key_far_above_its_lanes_first_keys(mean):
     say(f"  max |diff| {err:.2e}")
 
 
+@pytest.mark.parametrize("mean", [False, True])
+def test_split_offsets_far_apart_between_chunks(mean):
+    # one recent row sees a key of ~104 nats in the first group of one item
+    # and its largest key, ~131 nats, deep inside a later item whose first
+    # keys are ordinary: the first item's offset then lies more than 126
+    # (log2 units) above the second's, whose sum is still far from overflow;
+    # merging the two must not lose the second item's sum
+    w = CASES["d128-r544"]
+    x = synth.make_layer(w, seed=19, device="cpu")
+    K = x["K"].float()
+    for h in range(w.Hkv):
+        y = x["q_win"][0, h * w.G].float()[0]
+        for j, nats in ((1024 + 5, 104.0), (2048 + 700, 131.0)):
+            K[0, h, j] = nats * np.sqrt(w.D) * y / y.norm() ** 2
+    x["K"] = K.to(torch.bfloat16).contiguous()
+    s_ref, lse_ref = oracle.score(x["K"], x["q_win"], x["beacons"], x["counts"], N=w.N, rope_cos=x["rope_cos"],
+                                  rope_sin=x["rope_sin"], threads=4, agg="mean" if mean else "max")
+    assert lse_ref[..., w.C].max() > 120.0, "the planted keys do not dominate their row"
+    say(f"row-split score, offsets far apart between items, mean={mean}")
+    s_gpu, lse_gpu = _score(w, x, mean)
+    err = assert_scores_close(s_gpu, s_ref, "scores")
+    assert_scores_close(lse_gpu, lse_ref, "row_lse")
+    assert np.all(s_gpu <= 1e-4)
+    say(f"  max |diff| {err:.2e}")
+
+
 def _away(y):
     """Unit vector whose dot product with every row of y is negative (linear
     programming: push the largest normalised dot product furthest below 0)."""
