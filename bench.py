@@ -255,7 +255,7 @@ def stages_measure(w, dev, reps=5):
         bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
                   rope_sin=x["rope_sin"])
         e[1].record()
-        bkv.topk(d, scores, kept)
+        bkv.topk(d, scores, kept, ws)
         e[2].record()
         bkv.compact(d, x["K"], x["V"], kept, ws)
         e[3].record()
@@ -529,37 +529,60 @@ def configs_measure(dev, reps=5):
         kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device=dev)
         scores = torch.empty(d.B, d.Hkv, d.N, device=dev)
         src_of = torch.empty_like(kept) if fill else None
-        t_ev, t_sc = [], []
+        t_ev, t_sc, t_tk, t_one = [], [], [], []
         for r in range(reps + 1):
             x["K"].copy_(K0)
             x["V"].copy_(V0)
             torch.cuda.synchronize()
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
             e[0].record()
             bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
                       rope_sin=x["rope_sin"])
             e[1].record()
-            bkv.topk(d, scores, kept)
+            bkv.topk(d, scores, kept, ws)
+            e[2].record()
             if fill:
                 bkv.compact_fill(d, x["K"], x["V"], kept, src_of, ws)
             else:
                 bkv.compact(d, x["K"], x["V"], kept, ws)
-            e[2].record()
+            e[3].record()
             torch.cuda.synchronize()
+            if not fill:  # the entry point itself (the fused launch where it applies)
+                x["K"].copy_(K0)
+                x["V"].copy_(V0)
+                torch.cuda.synchronize()
+                f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                f0.record()
+                bkv.evict(d, x["K"], x["V"], x["q_win"], x["beacons"], x["counts"], ws, kept=kept, scores=scores,
+                          rope_cos=x["rope_cos"], rope_sin=x["rope_sin"])
+                f1.record()
+                torch.cuda.synchronize()
             if r:  # the first is a warm-up
-                t_ev.append(e[0].elapsed_time(e[2]) * 1e3)
+                t_ev.append(e[0].elapsed_time(e[3]) * 1e3)
                 t_sc.append(e[0].elapsed_time(e[1]) * 1e3)
+                t_tk.append(e[1].elapsed_time(e[2]) * 1e3)
+                if not fill:
+                    t_one.append(f0.elapsed_time(f1) * 1e3)
         assert bkv.device_status(ws) == bkv.OK
-        t = sorted(t_ev)[len(t_ev) // 2]
-        ts = sorted(t_sc)[len(t_sc) // 2]
+        med = lambda v: sorted(v)[len(v) // 2]
+        t, ts, tt = med(t_ev), med(t_sc), med(t_tk)
         es = 2 if w.dtype == "bf16" else 4
         kbytes = d.B * d.Hkv * w.N * (w.D * es + 4)
+        R = w.C + w.G * w.W
+        flops = 2 * 2 * d.B * d.Hkv * w.N * R * w.D  # both passes of the score, algorithmic rows
         res[name] = {"B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "N": w.N, "W": w.W, "C": w.C,
-                     "budget": w.budget, "R": w.C + w.G * w.W, "dtype": w.dtype,
+                     "budget": w.budget, "R": R, "dtype": w.dtype,
                      "compaction": "hole-filling" if fill else "order-preserving",
                      "eviction_latency_us": round(t, 1), "rows_per_s": round(d.B * d.Hkv * w.N / (t * 1e-6), 1),
-                     "score_us": round(ts, 1), "score_frac_of_hbm_peak": round(kbytes / (ts * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
-        print(f"# config {name}: eviction {t:.1f} us, score {ts:.1f} us", file=sys.stderr, flush=True)
+                     "score_us": round(ts, 1), "topk_us": round(tt, 1),
+                     "score_frac_of_hbm_peak": round(kbytes / (ts * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "score_tflops": round(flops / (ts * 1e-6) / 1e12, 1),
+                     "score_frac_of_mfma_peak": (round(flops / (ts * 1e-6) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)
+                                                 if w.dtype == "bf16" else None)}
+        if t_one:
+            res[name]["bkv_evict_us"] = round(med(t_one), 1)
+        print(f"# config {name}: eviction {t:.1f} us (bkv_evict {res[name].get('bkv_evict_us')}), score {ts:.1f} us, "
+              f"top-k {tt:.1f} us", file=sys.stderr, flush=True)
         del x, K0, V0, ws, kept, scores
         torch.cuda.empty_cache()
     return res

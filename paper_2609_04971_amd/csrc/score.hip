@@ -1867,8 +1867,12 @@ hipError_t launch_score(const bkv_dims& d, const WsLayout& L, int flags, const v
 // Shorter heads have few score items per head, so the selection and
 // compaction items come at the end of the grid and run with little to
 // overlap (the 4224-token steady state measured 217 us fused against 210
-// chained); longer heads take the selection's streaming path.
-bool evict_fusable(const bkv_dims& d, const WsLayout& L) { return L.rtg > 0 && L.nch >= 16 && d.N <= 32768; }
+// chained); longer heads take the selection's streaming path; heads of
+// several row groups leave the score items long and few (the R = 464 16K
+// layer measured 293 us fused against 213 chained).
+bool evict_fusable(const bkv_dims& d, const WsLayout& L) {
+    return L.rtg > 0 && L.R_pad_max == L.rtg * 16 && L.nch >= 16 && d.N <= 32768;
+}
 
 hipError_t launch_evict_fused(const bkv_dims& d, const WsLayout& L, int flags, void* K, void* V, const void* q_win,
                               const float* beacons, const int32_t* counts, const float* rope_cos,

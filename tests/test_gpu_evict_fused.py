@@ -25,8 +25,10 @@ from paper_2609_04971_amd import synth
 pytestmark = pytest.mark.gpu
 
 W = synth.Workload
-# the fused launch serves bf16 heads of 16K to 32K tokens (the chained calls
-# take the others), so every case has N in that range
+# the fused launch serves bf16 heads of 16K to 32K tokens whose rows fit one
+# register group (the chained calls take the others), so nearly every case
+# is of that kind; the four-row-group cases check that such heads, taken by
+# the chained calls inside bkv_evict, give the same result
 CASES = {
     "ragged": W("f1", B=2, Hq=8, Hkv=2, D=128, N=20001, W=8, C=4, budget=3000, revisit_frac=0.1),
     "prefix": W("f2", B=2, Hq=8, Hkv=2, D=128, N=16384, W=16, C=8, budget=2000, n_prefix=5),
