@@ -81,6 +81,9 @@ def parse():
     ap.add_argument("--no-trace", action="store_true", help="skip the periodic-eviction cycle timing")
     ap.add_argument("--no-diag", action="store_true", help="skip the synthetic quality diagnostics")
     ap.add_argument("--no-configs", action="store_true", help="skip the eviction timing of the other workloads")
+    ap.add_argument("--only-config", default=None,
+                    help="time only this other workload shape (a name of the configs section) and print its "
+                         "figures as one JSON line; for profiling a single shape")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -99,6 +102,11 @@ def main():
 
     import paper_2609_04971_amd as bkv
     from paper_2609_04971_amd import synth
+
+    if args.only_config:
+        torch.cuda.set_device(0)
+        print(json.dumps(configs_measure(torch.device("cuda:0"), only=args.only_config)), flush=True)
+        return
 
     w = synth.QWEN3_4B_32K
     L = args.layers or w.layers
@@ -502,7 +510,7 @@ def decode_trace_measure(w, dev, cycles=2, steady_extra=128):
     return res
 
 
-def configs_measure(dev, reps=5):
+def configs_measure(dev, reps=5, only=None):
     """Eviction latency of one layer (bkv_evict: score, top-k, compaction) on
     each workload shape besides the benchmark's cold 32K layer: the small
     fp32 case, the 4K layer, the steady-state eviction of the benchmark's
@@ -520,6 +528,10 @@ def configs_measure(dev, reps=5):
               ("qwen3-4b-steady-N4224-to-4096", steady, False),
               ("qwen3-4b-steady-N4224-to-4096-holefill", steady, True),
               ("qwen2.5-7b-N16384-gqa7", synth.QWEN25_7B_16K, False), ("llama-8b-N65536", synth.LLAMA8B_64K, False)]
+    if only is not None:
+        shapes = [t for t in shapes if t[0] == only]
+        if not shapes:
+            raise SystemExit(f"unknown config {only!r}")
     res = {}
     for name, w, fill in shapes:
         d = bkv.dims(B=w.B, Hq=w.Hq, Hkv=w.Hkv, D=w.D, N=w.N, W=w.W, C=w.C, budget=w.budget, dtype=w.dtype)
