@@ -84,7 +84,7 @@ constexpr int kFastTiles = 9;
 // for which the regions are laid out, and the shortest head it takes.
 constexpr int kTkHeadWords = 4;
 constexpr int kTkMaxSlices = 64;
-constexpr int kTkMaxHeads = 128;
+constexpr int kTkMaxHeads = 64;
 constexpr int kTkMinN = 8192;
 constexpr int kFastRowGroups = 8;
 
