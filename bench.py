@@ -84,6 +84,10 @@ def parse():
     ap.add_argument("--only-config", default=None,
                     help="time only this other workload shape (a name of the configs section) and print its "
                          "figures as one JSON line; for profiling a single shape")
+    ap.add_argument("--only-stages", action="store_true",
+                    help="time only the 32K layer's stages one by one (score, top-k, compaction, fused eviction; "
+                         "10 repetitions) and the scoring options, print them as one JSON line; for profiling "
+                         "those kernels alone")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -120,6 +124,15 @@ def main():
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
+
+    if args.only_stages:
+        res = {"stages": stages_measure(w, dev, reps=10)}
+        lay = [synth.make_layer(w, seed=l, device=dev) for l in range(6)]
+        ws = bkv.workspace(d, bkv.OP_EVICT)
+        scores = torch.empty(d.B, d.Hkv, d.N, device=dev)
+        res["score_options"] = score_options_measure(d, lay, scores, ws, d.P * d.N * (w.D * 2 + 4))
+        print(json.dumps(res), flush=True)
+        return
 
     # ---- resident synthetic stack (untimed) ---------------------------------
     t_gen = time.time()
@@ -183,7 +196,7 @@ def main():
     evict_med = statistics.median(evict_us)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
-                "kernel": "eviction launch: rows_kernel<128> + evict_kernel<128, 9, false>",
+                "kernel": "eviction launch: rows_kernel<128> + evict_kernel<128, 9, false, false>",
                 "algorithmic_bytes": evict_bytes, "moved_rows": moved,
                 "launch_us_mean": round(avg_us["evict"], 1),
                 "mfma_tflops": round(evict_flops / evict_s / 1e12, 1),
