@@ -338,7 +338,13 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
         });
     }
 #endif
-    auto bin_of = [&](float x) { return (int)fminf(fmaxf(floorf((x + 32.0f) * kBS), 0.f), (float)(BINS - 1)); };
+    // each key's bin, computed once (the scores themselves are not needed
+    // again: the threshold bin's members are re-read)
+    int bn[PER];
+    dev::static_for<PER>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        bn[i] = (int)fminf(fmaxf(floorf((v[i] + 32.0f) * kBS), 0.f), (float)(BINS - 1));
+    });
     // per-key flags as bits of masks built once, and integer arithmetic in the
     // per-key loops (comparisons there would become branches and masks)
     auto range_mask = [](int q, int a, int b) {  // bits i - 32 q of i in [a, b)
@@ -365,8 +371,7 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
         __syncthreads();
         dev::static_for<PER>([&](auto ic) {  // non-candidates count in the spare bin BINS
             constexpr int i = decltype(ic)::value;
-            const int b = bin_of(v[i]);  // computed for every key: no branch per key
-            atomicAdd(&sl.hist[BINS + (b - BINS) * (int)bit(cm, i)], 1);
+            atomicAdd(&sl.hist[BINS + (bn[i] - BINS) * (int)bit(cm, i)], 1);
         });
         __syncthreads();
         find_from_top<BINS / kNT>(sl.hist, ksel, sl);
@@ -379,7 +384,7 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
         for (int q = 0; q < PER / 32; ++q) mm[q] = 0;
         dev::static_for<PER>([&](auto ic) {
             constexpr int i = decltype(ic)::value;
-            mm[i / 32] |= (bit(cm, i) & eq(bin_of(v[i]), bstar)) << (i % 32);
+            mm[i / 32] |= (bit(cm, i) & eq(bn[i], bstar)) << (i % 32);
         });
         const ScoreRow row(srow, N);
 #pragma unroll
@@ -417,7 +422,7 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
     int n = nmem;
     dev::static_for<PER>([&](auto ic) {
         constexpr int i = decltype(ic)::value;
-        const uint32_t k = bit(fm, i) | (bit(cm, i) & gt(bin_of(v[i]), bstar));
+        const uint32_t k = bit(fm, i) | (bit(cm, i) & gt(bn[i], bstar));
         km[i / 32] |= k << (i % 32);
         n += (int)k;
     });
@@ -430,7 +435,21 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
         }
     }
     int total;
-    int pos = block_scan(n, sl.scan, &total);
+    int pos = block_scan(n, sl.scan, &total);  // ends with a barrier: the bitmap is read
+    if (budget <= BINS) {
+        // the kept tokens in output order in LDS, then stored coalesced
+        int* stage = sl.hist;
+#pragma unroll
+        for (int q = 0; q < PER / 32; ++q) {
+            for (uint32_t m = km[q]; m; m &= m - 1) {
+                if (pos < budget) stage[pos] = j0 + 32 * q + __builtin_ctz(m);
+                ++pos;
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < min(total, budget); i += kNT) dev::st_flag(out + i, stage[i]);
+        return true;
+    }
 #pragma unroll
     for (int q = 0; q < PER / 32; ++q) {
         for (uint32_t m = km[q]; m; m &= m - 1) {
@@ -441,7 +460,7 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
     return true;
 }
 
-// One head's selection; see select_reg and select_stream.
+// One head's selection; see select_bins and select_stream.
 template <int BINS>
 __device__ void select_item(const float* srow, int32_t* out, int N, int budget, int W, int n_prefix,
                             SelLds<BINS>& sl) {
