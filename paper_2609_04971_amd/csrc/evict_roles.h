@@ -462,7 +462,7 @@ __device__ bool select_bins(const float* srow, int32_t* out, int N, int budget, 
 
 // One head's selection; see select_bins and select_stream.
 template <int BINS>
-__device__ void select_item(const float* srow, int32_t* out, int N, int budget, int W, int n_prefix,
+__device__ __forceinline__ void select_item(const float* srow, int32_t* out, int N, int budget, int W, int n_prefix,
                             SelLds<BINS>& sl) {
     if (N <= budget) {
         for (int i = threadIdx.x; i < N; i += kNT) dev::st_flag(out + i, i);
@@ -485,7 +485,7 @@ constexpr int kSegF = 256;  // compaction rows per fused work item
 // Returns false if the kept indices are not strictly ascending within
 // [0, N) (the segment then moves nothing).  s_src holds kSegF ints.
 template <int RB>
-__device__ bool compact_item(char* Kh, char* Vh, const int32_t* kh, int* flags, int seg, int n_keep, int N,
+__device__ __forceinline__ bool compact_item(char* Kh, char* Vh, const int32_t* kh, int* flags, int seg, int n_keep, int N,
                              int* s_src, int* s_bits, int* hdr) {
     constexpr int VPR = RB / 16;
     constexpr int NV = 2 * kSegF * VPR / kNT;  // 16-byte vectors per thread (K and V)
