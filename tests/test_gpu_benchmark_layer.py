@@ -149,3 +149,42 @@ def test_wide_group_layers_sampled_heads(w):
         band, diff = compare_kept(kg[None], kr[None], ref["scores"][lb, h][None], w.N, w.W, 0, w.budget)
         say(f"  head ({b}, {h}): tie band {band}, {diff} in-band differences")
         assert_rows_match(host(x["K"][b, h])[None], ref["K"][lb, h][None], kg[None], kr[None], d.n_keep, "K")
+
+
+def test_stacked_layers_steady_state_sampled_heads():
+    # the decode trace's eviction: several layers stacked into the batch of
+    # one call (here 12 layers of the Qwen3-4B shape, B = 192, 1536 heads),
+    # at the steady state 4224 -> 4096 tokens; every head's properties, and
+    # sampled heads (first, last, and layer boundaries) against the oracle
+    w = synth.QWEN3_4B_32K.with_(B=16 * 12, N=4224)
+    d = dims_of(w)
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    kept = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
+    scores = torch.empty(d.B, d.Hkv, d.N, device="cuda")
+    x = synth.make_layer(w, seed=300, device="cuda")
+    heads = [(0, 0), (15, 7), (16, 0), (100, 3), (191, 7)]
+    bsel = sorted({b for b, _ in heads})
+    xh = {k: (host(v[bsel]) if k in ("K", "V", "q_win", "beacons", "counts") else host(v)) for k, v in x.items()}
+    say(f"stacked layers: {d}")
+    bkv.evict(d, x["K"], x["V"], x["q_win"], x["beacons"], x["counts"], ws, kept=kept, scores=scores,
+              rope_cos=x["rope_cos"], rope_sin=x["rope_sin"])
+    torch.cuda.synchronize()
+    assert bkv.device_status(ws) == bkv.OK
+    s_all, k_all = host(scores).numpy(), host(kept).numpy()
+    assert not np.isnan(s_all).any() and np.all(s_all <= 1e-4)
+    assert np.all(np.diff(k_all, axis=-1) > 0)
+    assert np.array_equal(k_all[..., -w.W:], np.broadcast_to(np.arange(w.N - w.W, w.N), k_all[..., -w.W:].shape))
+    say(f"  isolation: oracle top-k on the GPU's scores, all {d.P} heads")
+    np.testing.assert_array_equal(oracle.topk(s_all.astype(np.float64), w.budget, w.W, 0), k_all)
+    hl = [(bsel.index(b), h) for b, h in heads]
+    say(f"  oracle on {len(hl)} heads")
+    ref = oracle.evict(xh["K"], xh["V"], xh["q_win"], xh["beacons"], xh["counts"], N=w.N, budget=w.budget, W=w.W,
+                       rope_cos=xh["rope_cos"], rope_sin=xh["rope_sin"], heads=hl, threads=len(hl))
+    for (b, h), (lb, _) in zip(heads, hl):
+        assert_scores_close(s_all[b, h], ref["scores"][lb, h])
+        kg, kr = k_all[b, h], ref["kept"][lb, h]
+        band, diff = compare_kept(kg[None], kr[None], ref["scores"][lb, h][None], w.N, w.W, 0, w.budget)
+        say(f"  head ({b}, {h}): tie band {band}, {diff} in-band differences")
+        K_gpu = host(x["K"][b, h])
+        assert_rows_match(K_gpu[None], ref["K"][lb, h][None], kg[None], kr[None], d.n_keep, "K")
+        assert np.array_equal(raw_bits(K_gpu)[: d.n_keep], raw_bits(xh["K"][lb, h])[kg])
