@@ -42,6 +42,9 @@ CASES = {
     # four row groups, one per wave (R = 16 + 7*64 = 464; D = 64: R = 16 + 4*107 = 444)
     "four-row-groups": W("f11", B=1, Hq=14, Hkv=2, D=128, N=16900, W=64, C=16, budget=2048, n_centroids=16),
     "four-row-groups-d64": W("f12", B=1, Hq=8, Hkv=2, D=64, N=16461, W=107, C=16, budget=1900, n_centroids=8),
+    # budgets above the selection's bin count: its kept tokens go out without the LDS staging
+    "budget-above-bins": W("f13", B=1, Hq=8, Hkv=2, D=128, N=24000, W=16, C=8, budget=6000),
+    "budget-above-bins-d64": W("f14", B=1, Hq=8, Hkv=2, D=64, N=20000, W=16, C=8, budget=3000),
 }
 
 
