@@ -60,3 +60,55 @@ def test_noalloc_options_and_internal_outputs():
     _both(SMALL, seed=63, mean=True, causal=True)
     _both(BIG, seed=64, outputs=False)
     _both(SMALL, seed=65, outputs=False)
+
+
+# its use case: callers that cannot allocate, such as code under HIP graph
+# capture.  The call is captured once and replayed several times, with the
+# program's own eager work and synchronisations between replays; every replay
+# is checked bit for bit against an eager call on the same inputs (one
+# layer on the chained calls, one on the fused launch).
+@pytest.mark.parametrize("w", [
+    W("na-graph", B=2, Hq=8, Hkv=2, D=128, N=3000, W=16, C=8, budget=700, n_prefix=4, revisit_frac=0.1),
+    W("na-graph-fused", B=2, Hq=8, Hkv=2, D=128, N=16384, W=16, C=8, budget=2048, revisit_frac=0.05),
+], ids=lambda w: w.name)
+def test_noalloc_graph_replays(w):
+    d = dims_of(w)
+    x = synth.make_layer(w, seed=71, device="cuda")
+    K0, V0 = x["K"].clone(), x["V"].clone()
+    args = (x["q_win"], x["beacons"], x["counts"])
+    rope = dict(rope_cos=x["rope_cos"], rope_sin=x["rope_sin"])
+    # eager reference
+    Kr, Vr = K0.clone(), V0.clone()
+    kept_r = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
+    scores_r = torch.empty(d.B, d.Hkv, d.N, device="cuda")
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    bkv.evict_noalloc(d, Kr, Vr, *args, kept=kept_r, scores=scores_r, status=status, **rope)
+    torch.cuda.synchronize()
+    assert int(status.item()) == bkv.OK
+    # captured call on static buffers
+    K, V = K0.clone(), V0.clone()
+    kept = torch.full_like(kept_r, -1)
+    scores = torch.full_like(scores_r, float("nan"))
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say(f"capture bkv_evict_noalloc {w.name}: {d}")
+    with torch.cuda.graph(g):
+        bkv.evict_noalloc(d, K, V, *args, kept=kept, scores=scores, status=status, **rope)
+    torch.cuda.synchronize()
+    for r in range(4):
+        # the program's own eager work between replays: fresh inputs, cleared outputs
+        K.copy_(K0)
+        V.copy_(V0)
+        kept.fill_(-1)
+        scores.fill_(float("nan"))
+        status.fill_(-1)
+        torch.cuda.synchronize()
+        say(f"  replay {r}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert int(status.item()) == bkv.OK
+        np.testing.assert_array_equal(kept.cpu().numpy(), kept_r.cpu().numpy())
+        assert torch.equal(scores, scores_r)
+        n = d.n_keep
+        assert np.array_equal(raw_bits(K)[..., :n, :], raw_bits(Kr)[..., :n, :])
+        assert np.array_equal(raw_bits(V)[..., :n, :], raw_bits(Vr)[..., :n, :])
