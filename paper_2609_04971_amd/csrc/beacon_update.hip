@@ -7,20 +7,20 @@
 // of largest cosine similarity (ties -> lowest slot, cosine 0 when a norm is
 // 0) and that slot moves to the running mean of its members.
 //
-// One workgroup of 256 threads per (batch, kv-head).  The head's beacons live
-// in LDS (rows padded to D + 4 floats so that sixteen lanes reading 16-byte
-// vectors of sixteen different slots hit distinct banks) together with their
-// squared norms, which are kept up to date as slots change.  All four waves
-// bring the beacons in (every 16-byte load of the head issued before any is
-// waited on: one HBM round trip) and compute the norms (four threads per
-// slot).  Then one wave takes the T*G queries of the head's group strictly
-// in order (t-major, then g), each seeing the previous update: lane c
-// accumulates slot c's dot product over D with 16-byte LDS reads; an argmax
-// over lanes (DPP, no LDS round trip) picks the slot; the lanes update that
-// slot's D coordinates and its norm in parallel.  Finally the four waves
-// write back the slots that changed (at most T*G of the C rows; the others
-// still hold what was read).  The LDS is sized by C, so small C leaves room
-// for more heads per CU.
+// One wave (a 64-thread workgroup) per (batch, kv-head): the queries of a
+// head are taken strictly in order, each seeing the previous update, so a
+// head's work is one sequential chain, and small workgroups let many heads'
+// chains run side by side on a compute unit (a layer-stacked call has
+// thousands of heads).  The head's beacons live in LDS (rows padded to
+// D + 4 floats) together with their squared norms, which are kept up to
+// date as slots change.  The wave brings the beacons in with up to eight
+// 16-byte loads per lane in flight, then computes the norms, four lanes per
+// slot.  Per query: lanes 4c .. 4c+3 each take a quarter of slot c's dot
+// product (16-byte LDS reads) and a quad sum completes it; an argmax over
+// the lanes (DPP, no LDS round trip) picks the slot; the lanes update that
+// slot's D coordinates and its norm in parallel.  Finally the wave writes
+// back the slots that changed (at most T*G of the C rows; the others still
+// hold what was read).  The LDS is sized by C.
 #include <math.h>
 
 #include "device_common.h"
@@ -34,58 +34,38 @@ namespace {
 __device__ __forceinline__ float widen(uint16_t v) { return dev::bf16_to_f32(v); }
 __device__ __forceinline__ float widen(float v) { return v; }
 
-// Dot product of two D-float rows in LDS (16-byte aligned), with four
-// independent partial sums so that the FMAs do not wait on each other.
-template <int D>
-__device__ __forceinline__ float row_dot(const float* a, const float* b) {
-    const float4* ar = reinterpret_cast<const float4*>(a);
-    const float4* br = reinterpret_cast<const float4*>(b);
-    float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
-#pragma unroll 8
-    for (int d4 = 0; d4 < D / 4; ++d4) {
-        const float4 u = ar[d4], v = br[d4];
-        p0 = fmaf(u.x, v.x, p0);
-        p1 = fmaf(u.y, v.y, p1);
-        p2 = fmaf(u.z, v.z, p2);
-        p3 = fmaf(u.w, v.w, p3);
-    }
-    return (p0 + p1) + (p2 + p3);
-}
-
-// Orders the calling wave's LDS accesses for the compiler: one lane's
-// write before the fence is seen by another lane's read after it.  A wave's
-// LDS instructions execute in order, so a wavefront-scope fence needs no
-// wait instruction; in particular it does not wait for the next query's
-// global loads in flight (a workgroup-scope fence or barrier would).  The
-// query loop runs on one wave while the others wait at a later barrier, so
-// it could not use the workgroup barrier anyway.
+// Orders the wave's LDS accesses for the compiler: one lane's write before
+// the fence is seen by another lane's read after it.  A wave's LDS
+// instructions execute in order, so a wavefront-scope fence needs no wait
+// instruction; in particular it does not wait for the next query's global
+// loads in flight (a workgroup-scope fence or barrier would).
 __device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 
-constexpr int kThreads = 256;
-constexpr int kMaxSlots = 64;  // the boundary rejects C > 64: one bit per slot in a 64-bit mask
+constexpr int kThreads = 64;    // one wave per head
+constexpr int kMaxSlots = 64;   // the boundary rejects C > 64: one bit per slot in a 64-bit mask
+constexpr int kLoadChunk = 8;   // 16-byte beacon loads in flight per lane
+static_assert(kMaxSlots <= kThreads, "one lane per slot holds its count and its dirty bit");
 
 // LDS bytes of one head: C padded beacon rows, the current query, C norms,
-// C counts, the mask of changed slots.
+// C counts.
 template <int D>
 constexpr size_t smem_bytes(int C) {
-    return ((size_t)C * (D + 4) + D + C) * sizeof(float) + (size_t)C * sizeof(int) + sizeof(unsigned long long);
+    return ((size_t)C * (D + 4) + D + C) * sizeof(float) + (size_t)C * sizeof(int);
 }
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void beacon_update_kernel(const T* __restrict__ q_new, int T_steps,
                                                                  float* beacons, int32_t* counts, int32_t* assign,
                                                                  int Hq, int Hkv, int C) {
-    constexpr int LD = D + 4;                         // padded row
-    constexpr int PER = D / 64;                       // coordinates per lane in lane-parallel loops
-    constexpr int kLoads = kMaxSlots * D / 4 / kThreads;  // 16-byte beacon loads per thread at most
+    constexpr int LD = D + 4;      // padded row
+    constexpr int PER = D / 64;    // coordinates per lane in lane-parallel loops
+    constexpr int QD = D / 4;      // coordinates per lane of a slot's dot product (four lanes per slot)
     extern __shared__ __attribute__((aligned(16))) float smem[];
-    float* bl = smem;                                 // [C][LD]
-    float* xs = bl + C * LD;                          // [D], 16-byte aligned: C * LD and D are multiples of 4
-    float* bn2 = xs + D;                              // [C] squared norm of each slot
-    int* cnt = reinterpret_cast<int*>(bn2 + C);       // [C]
-    unsigned long long* dirty_out = reinterpret_cast<unsigned long long*>(cnt + C);  // 8-byte aligned
-    const int tid = threadIdx.x, lane = tid & 63;
-    const bool seq_wave = tid < 64;
+    float* bl = smem;                            // [C][LD]
+    float* xs = bl + C * LD;                     // [D], 16-byte aligned: C * LD and D are multiples of 4
+    float* bn2 = xs + D;                         // [C] squared norm of each slot
+    int* cnt = reinterpret_cast<int*>(bn2 + C);  // [C]
+    const int lane = threadIdx.x;
     const int h = blockIdx.x, b = h / Hkv, kh = h % Hkv;
     const int G = Hq / Hkv;
     float* bh = beacons + (size_t)h * C * D;
@@ -94,37 +74,40 @@ __global__ __launch_bounds__(kThreads) void beacon_update_kernel(const T* __rest
         const int t = qq / G, g = qq - t * G;
         return q_new + (((size_t)b * Hq + (size_t)kh * G + g) * T_steps + t) * D;
     };
-    // The first query, the counts and every beacon vector of the head are
-    // loaded unconditionally (threads past the end re-read the last element)
-    // and pinned by an empty asm before the first store uses them, so the
-    // compiler can neither sink a load into the guarded store nor wait
-    // between loads: all of them issue before the first wait.
+    // The first query, the counts and a chunk of beacon vectors are loaded
+    // unconditionally (lanes past the end re-read the last element) and
+    // pinned by an empty asm before the first store uses them, so the
+    // compiler neither sinks a load into the guarded store nor waits
+    // between loads: a chunk's loads all issue before the first wait.
     T xnext[PER];
 #pragma unroll
     for (int k = 0; k < PER; ++k) xnext[k] = query_ptr(0)[lane + 64 * k];
-    const int n4 = C * D / 4;
-    dev::u32x4 v[kLoads];
-#pragma unroll
-    for (int k = 0; k < kLoads; ++k) v[k] = reinterpret_cast<const dev::u32x4*>(bh)[min(tid + kThreads * k, n4 - 1)];
-    int cv = counts[(size_t)h * C + min(tid, C - 1)];
-#pragma unroll
-    for (int k = 0; k < kLoads; ++k) asm volatile("" : "+v"(v[k]));
+    int cv = counts[(size_t)h * C + min(lane, C - 1)];
     asm volatile("" : "+v"(cv));
+    const int n4 = C * D / 4;
+    for (int base = 0; base < n4; base += kThreads * kLoadChunk) {
+        dev::u32x4 v[kLoadChunk];
 #pragma unroll
-    for (int k = 0; k < kLoads; ++k) {
-        const int i = tid + kThreads * k;
-        if (i < n4) *reinterpret_cast<dev::u32x4*>(&bl[(4 * i) / D * LD + (4 * i) % D]) = v[k];
+        for (int k = 0; k < kLoadChunk; ++k)
+            v[k] = reinterpret_cast<const dev::u32x4*>(bh)[min(base + lane + kThreads * k, n4 - 1)];
+#pragma unroll
+        for (int k = 0; k < kLoadChunk; ++k) asm volatile("" : "+v"(v[k]));
+#pragma unroll
+        for (int k = 0; k < kLoadChunk; ++k) {
+            const int i = base + lane + kThreads * k;
+            if (i < n4) *reinterpret_cast<dev::u32x4*>(&bl[(4 * i) / D * LD + (4 * i) % D]) = v[k];
+        }
     }
-    if (tid < C) cnt[tid] = cv;
-    __syncthreads();
-    // squared norms: four threads (one quad) per slot, D/4 coordinates each
-    {
-        const int c = tid >> 2, part = tid & 3;
+    if (lane < C) cnt[lane] = cv;
+    wave_lds_fence();
+    // squared norms: four lanes per slot, sixteen slots at a time
+    for (int c0 = 0; c0 < C; c0 += kThreads / 4) {
+        const int c = c0 + (lane >> 2), part = lane & 3;
         float p = 0.f;
         if (c < C) {
-            const float4* r = reinterpret_cast<const float4*>(&bl[c * LD + part * (D / 4)]);
+            const float4* r = reinterpret_cast<const float4*>(&bl[c * LD + part * QD]);
 #pragma unroll
-            for (int d4 = 0; d4 < D / 16; ++d4) {
+            for (int d4 = 0; d4 < QD / 4; ++d4) {
                 const float4 u = r[d4];
                 p = fmaf(u.x, u.x, p);
                 p = fmaf(u.y, u.y, p);
@@ -135,75 +118,90 @@ __global__ __launch_bounds__(kThreads) void beacon_update_kernel(const T* __rest
         p = dev::quad_sum(p);
         if (c < C && part == 0) bn2[c] = p;
     }
-    __syncthreads();
+    wave_lds_fence();
 
-    if (seq_wave) {
-        unsigned long long dirty = 0;  // slots changed (wave-uniform)
-        for (int q = 0; q < nq; ++q) {
-            float xn = 0.f;
+    unsigned long long dirty = 0;  // slots changed (wave-uniform)
+    for (int q = 0; q < nq; ++q) {
+        float xn = 0.f;
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const float x = widen(xnext[k]);
+            xs[lane + 64 * k] = x;
+            xn = fmaf(x, x, xn);
+        }
+        // the next query (the last one again at the end: no branch to join,
+        // so nothing waits for it before its use)
+#pragma unroll
+        for (int k = 0; k < PER; ++k) xnext[k] = query_ptr(min(q + 1, nq - 1))[lane + 64 * k];
+        xn = dev::wave_sum(xn);
+        wave_lds_fence();
+        // lowest empty slot, if any
+        const unsigned long long empty = __ballot(lane < C && cnt[lane] == 0);
+        int chosen;
+        if (empty) {
+            chosen = __ffsll(empty) - 1;
+#pragma unroll
+            for (int k = 0; k < PER; ++k) bl[chosen * LD + lane + 64 * k] = xs[lane + 64 * k];
+            if (lane == 0) {
+                cnt[chosen] = 1;
+                bn2[chosen] = xn;
+            }
+        } else {
+            // argmax over the slots, ties -> lowest slot: the minimum of
+            // (inverted order key of the cosine, slot)
+            unsigned long long best = ~0ull;
+            for (int c0 = 0; c0 < C; c0 += kThreads / 4) {
+                const int c = c0 + (lane >> 2), part = lane & 3;
+                float dot = 0.f;
+                if (c < C) {
+                    const float4* ar = reinterpret_cast<const float4*>(&bl[c * LD + part * QD]);
+                    const float4* xr = reinterpret_cast<const float4*>(&xs[part * QD]);
+                    float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
+#pragma unroll
+                    for (int d4 = 0; d4 < QD / 4; ++d4) {
+                        const float4 u = ar[d4], v = xr[d4];
+                        p0 = fmaf(u.x, v.x, p0);
+                        p1 = fmaf(u.y, v.y, p1);
+                        p2 = fmaf(u.z, v.z, p2);
+                        p3 = fmaf(u.w, v.w, p3);
+                    }
+                    dot = (p0 + p1) + (p2 + p3);
+                }
+                dot = dev::quad_sum(dot);
+                const float bn = (c < C) ? bn2[c] : 0.f;
+                const float cs = (xn == 0.f || bn == 0.f) ? 0.f : dot / (sqrtf(xn) * sqrtf(bn));
+                const unsigned long long key =
+                    (c < C && part == 0) ? ((unsigned long long)(~dev::ord_key(cs)) << 32) | (unsigned)c : ~0ull;
+                best = key < best ? key : best;
+            }
+            chosen = (int)(unsigned)dev::wave_min_u64(best);
+            const int n = cnt[chosen] + 1;
+            const float inv = 1.0f / (float)n;
+            float p = 0.f;
 #pragma unroll
             for (int k = 0; k < PER; ++k) {
-                const float x = widen(xnext[k]);
-                xs[lane + 64 * k] = x;
-                xn = fmaf(x, x, xn);
+                const int d = lane + 64 * k;
+                const float bv = bl[chosen * LD + d];
+                const float nv = bv + (xs[d] - bv) * inv;
+                bl[chosen * LD + d] = nv;
+                p = fmaf(nv, nv, p);
             }
-            // the next query (the last one again at the end: no branch to
-            // join, so nothing waits for it before its use)
-#pragma unroll
-            for (int k = 0; k < PER; ++k) xnext[k] = query_ptr(min(q + 1, nq - 1))[lane + 64 * k];
-            xn = dev::wave_sum(xn);
-            wave_lds_fence();
-            // lowest empty slot, if any
-            const unsigned long long empty = __ballot(lane < C && cnt[lane] == 0);
-            int chosen;
-            if (empty) {
-                chosen = __ffsll(empty) - 1;
-#pragma unroll
-                for (int k = 0; k < PER; ++k) bl[chosen * LD + lane + 64 * k] = xs[lane + 64 * k];
-                if (lane == 0) {
-                    cnt[chosen] = 1;
-                    bn2[chosen] = xn;
-                }
-            } else {
-                const float dot = (lane < C) ? row_dot<D>(&bl[lane * LD], xs) : 0.f;
-                const float bn = (lane < C) ? bn2[lane] : 0.f;
-                const float cs = (xn == 0.f || bn == 0.f) ? 0.f : dot / (sqrtf(xn) * sqrtf(bn));
-                // argmax over the slots, ties -> lowest slot: the minimum of
-                // (inverted order key of the cosine, slot)
-                const unsigned long long key =
-                    lane < C ? ((unsigned long long)(~dev::ord_key(cs)) << 32) | (unsigned)lane : ~0ull;
-                chosen = (int)(unsigned)dev::wave_min_u64(key);
-                const int n = cnt[chosen] + 1;
-                const float inv = 1.0f / (float)n;
-                float p = 0.f;
-#pragma unroll
-                for (int k = 0; k < PER; ++k) {
-                    const int d = lane + 64 * k;
-                    const float bv = bl[chosen * LD + d];
-                    const float nv = bv + (xs[d] - bv) * inv;
-                    bl[chosen * LD + d] = nv;
-                    p = fmaf(nv, nv, p);
-                }
-                p = dev::wave_sum(p);
-                if (lane == 0) {
-                    cnt[chosen] = n;
-                    bn2[chosen] = p;
-                }
+            p = dev::wave_sum(p);
+            if (lane == 0) {
+                cnt[chosen] = n;
+                bn2[chosen] = p;
             }
-            dirty |= 1ull << chosen;
-            if (assign && lane == 0) assign[(size_t)h * T_steps * G + q] = chosen;
-            wave_lds_fence();
         }
-        if (lane == 0) *dirty_out = dirty;
+        dirty |= 1ull << chosen;
+        if (assign && lane == 0) assign[(size_t)h * T_steps * G + q] = chosen;
+        wave_lds_fence();
     }
-    __syncthreads();
     // write back the changed slots only: the others still hold what was read
-    const unsigned long long dirty = *dirty_out;
-    for (int i = tid; i < n4; i += kThreads) {
+    for (int i = lane; i < n4; i += kThreads) {
         const int c = (4 * i) / D, d = (4 * i) % D;
         if ((dirty >> c) & 1ull) reinterpret_cast<float4*>(bh)[i] = *reinterpret_cast<const float4*>(&bl[c * LD + d]);
     }
-    if (tid < C && ((dirty >> tid) & 1ull)) counts[(size_t)h * C + tid] = cnt[tid];
+    if (lane < C && ((dirty >> lane) & 1ull)) counts[(size_t)h * C + lane] = cnt[lane];
 }
 
 }  // namespace
