@@ -45,7 +45,7 @@ enum HeadWord : int {
 
 enum DevErr : int { kErrScoreWait = 1, kErrCompactWait = 2, kErrStamp = 4, kErrBadIndex = 8 };
 
-constexpr int kSegRows = 64;  // compaction rows per work item
+constexpr int kSegRows = 128;  // compaction rows per work item
 constexpr int kMaxFillKeep = 65536;  // hole-filling compaction: kept rows per head at most (LDS bitmap)
 
 // Per-head row metadata written before scoring: word 0 = number of occupied

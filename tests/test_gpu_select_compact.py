@@ -149,7 +149,8 @@ COMPACT = [
     (1, 3, 777, 777, 64, torch.bfloat16, 300),
     (1, 2, 300, 300, 128, torch.float32, 100),
     (2, 4, 4096, 4096, 128, torch.bfloat16, 2048),
-    (1, 2, 130, 130, 128, torch.bfloat16, 65),  # one full segment + a 1-row segment
+    (1, 2, 130, 130, 128, torch.bfloat16, 65),    # one partial segment
+    (1, 2, 300, 300, 128, torch.bfloat16, 129),   # one full 128-row segment + a 1-row segment
 ]
 
 
@@ -217,5 +218,5 @@ def test_compact_rejects_non_ascending_kept():
     Kr, Vr = oracle.compact(K0[:, :1], V0[:, :1], kept[:, :1].numpy())
     np.testing.assert_array_equal(raw_bits(Kd[:, :1]), Kr.view(np.uint16))
     np.testing.assert_array_equal(raw_bits(Vd[:, :1]), Vr.view(np.uint16))
-    # the first segment of head 1 (rows 0..63) holds the bad pair: untouched
-    np.testing.assert_array_equal(raw_bits(Kd[0, 1, :64]), raw_bits(K0[0, 1, :64]))
+    # the segment of head 1 holding the bad pair (rows 0..127, the whole head here): untouched
+    np.testing.assert_array_equal(raw_bits(Kd[0, 1, :budget]), raw_bits(K0[0, 1, :budget]))
