@@ -461,7 +461,9 @@ def decode_trace_measure(w, dev, cycles=2, steady_extra=128):
     events on the launch stream; also the wall time per step (host and
     device, Python launches included).  The decode model itself (attention,
     MLP, appending K/V) is not part of the method's path and is not run:
-    the cache rows past 4096 keep what the previous cycle left there."""
+    the cache rows past 4096 keep what the previous cycle left there.
+    The same evictions are then timed with the hole-filling compaction
+    (score, top-k and bkv_compact_fill, three calls over the stacked batch)."""
     import torch
 
     import paper_2609_04971_amd as bkv
@@ -503,9 +505,28 @@ def decode_trace_measure(w, dev, cycles=2, steady_extra=128):
         walls.append(wall)
         bu_us += [e0.elapsed_time(e1) * 1e3 for k, e0, e1 in ev if k == "bu"]
         ev_us += [e0.elapsed_time(e1) * 1e3 for k, e0, e1 in ev if k == "ev"]
+    # The same cycles with the hole-filling compaction (bkv_score, bkv_topk,
+    # bkv_compact_fill over the same stacked batch): the kept rows below
+    # 4096 stay where they are and only the kept rows past it move into the
+    # holes.  The beacon updates are the same calls as above and are not
+    # repeated.
+    scores = torch.empty(dB.B, dB.Hkv, dB.N, dtype=torch.float32, device=dev)
+    sel = torch.empty_like(kept)
+    fill_us = []
+    for c in range(cycles + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        bkv.score(dB, X["K"], X["q_win"], beacons, counts, scores, ws, rope_cos=X["rope_cos"], rope_sin=X["rope_sin"])
+        bkv.topk(dB, scores, sel, ws)
+        bkv.compact_fill(dB, X["K"], X["V"], sel, kept, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        if c > 0:
+            fill_us.append(e0.elapsed_time(e1) * 1e3)
     if bkv.device_status(ws) != bkv.OK:
         raise SystemExit("device status after the decode trace")
     bu = statistics.mean(bu_us)
+    fill_cycle = statistics.mean(fill_us)
     ev_cycle = statistics.mean(ev_us)
     ev_step = sum(ev_us) / steps
     res = {"layers": L, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "C": w.C, "W": w.W,
@@ -516,8 +537,12 @@ def decode_trace_measure(w, dev, cycles=2, steady_extra=128):
            "evict_us_per_layer": round(ev_cycle / L, 1),
            "evict_us_per_step": round(ev_step, 2),
            "device_us_per_step": round(bu + ev_step, 2),
-           "wall_us_per_step": round(sum(walls) * 1e6 / steps, 1)}
-    del X, beacons, counts, q_steps, ws, kept
+           "wall_us_per_step": round(sum(walls) * 1e6 / steps, 1),
+           "hole_filling": {"calls": "bkv_score, bkv_topk, bkv_compact_fill over the same stacked batch",
+                            "evict_us_per_cycle": round(fill_cycle, 1),
+                            "evict_us_per_step": round(fill_cycle / steady_extra, 2),
+                            "device_us_per_step": round(bu + fill_cycle / steady_extra, 2)}}
+    del X, beacons, counts, q_steps, ws, kept, scores, sel
     torch.cuda.empty_cache()
     print(f"# decode trace: {res}", file=sys.stderr, flush=True)
     return res
