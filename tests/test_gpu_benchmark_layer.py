@@ -4,7 +4,11 @@ same calls bench.py times (score -> top-k -> compact on one workspace).
 Every head of one layer is checked against the oracle (scores, kept set,
 and the selection and compaction in isolation, bit for bit); a second layer
 through the same workspace is checked on sampled heads; properties that hold
-at any size are checked on every head."""
+at any size are checked on every head.  The decode trace's evictions (12
+Qwen3-4B layers stacked into one call at the steady state 4224 -> 4096, with
+the fused launch and with the hole-filling compaction) and the wide-group
+layers are checked on sampled heads, with every head's selection in
+isolation."""
 import numpy as np
 import pytest
 import torch
@@ -188,3 +192,61 @@ def test_stacked_layers_steady_state_sampled_heads():
         K_gpu = host(x["K"][b, h])
         assert_rows_match(K_gpu[None], ref["K"][lb, h][None], kg[None], kr[None], d.n_keep, "K")
         assert np.array_equal(raw_bits(K_gpu)[: d.n_keep], raw_bits(xh["K"][lb, h])[kg])
+
+
+def test_stacked_layers_steady_state_hole_filling():
+    # the decode trace's eviction with the hole-filling compaction, as timed:
+    # bkv_score, bkv_topk and bkv_compact_fill over 12 stacked layers of the
+    # Qwen3-4B shape (B = 192, 1536 heads) at the steady state 4224 -> 4096.
+    #  * every head: the oracle's selection on the GPU's own scores gives the
+    #    GPU's kept set bit for bit; src_of holds that set, and each row below
+    #    4096 of K and V is, bit for bit, the old row src_of names;
+    #  * sampled heads: scores against the oracle, and the oracle's
+    #    hole-filling compaction of the GPU's kept set gives the GPU's K, V
+    #    (all 4224 rows) and src_of bit for bit
+    w = synth.QWEN3_4B_32K.with_(B=16 * 12, N=4224)
+    d = dims_of(w)
+    ws = bkv.workspace(d, bkv.OP_EVICT)
+    sel = torch.empty(d.B, d.Hkv, d.n_keep, dtype=torch.int32, device="cuda")
+    src_of = torch.empty_like(sel)
+    scores = torch.empty(d.B, d.Hkv, d.N, device="cuda")
+    x = synth.make_layer(w, seed=301, device="cuda")
+    heads = [(0, 0), (15, 7), (16, 0), (100, 3), (191, 7)]
+    bsel = sorted({b for b, _ in heads})
+    xh = {k: (host(v[bsel]) if k in ("K", "V", "q_win", "beacons", "counts") else host(v)) for k, v in x.items()}
+    K0, V0 = x["K"].clone(), x["V"].clone()
+    say(f"stacked layers, hole filling: {d}")
+    bkv.score(d, x["K"], x["q_win"], x["beacons"], x["counts"], scores, ws, rope_cos=x["rope_cos"],
+              rope_sin=x["rope_sin"])
+    bkv.topk(d, scores, sel, ws)
+    bkv.compact_fill(d, x["K"], x["V"], sel, src_of, ws)
+    torch.cuda.synchronize()
+    assert bkv.device_status(ws) == bkv.OK
+    s_all, k_all, so_all = host(scores).numpy(), host(sel).numpy(), host(src_of).numpy()
+    assert not np.isnan(s_all).any() and np.all(s_all <= 1e-4)
+    say(f"  isolation: oracle top-k on the GPU's scores, all {d.P} heads")
+    np.testing.assert_array_equal(oracle.topk(s_all.astype(np.float64), w.budget, w.W, 0), k_all)
+    assert np.array_equal(np.sort(so_all, axis=-1), k_all)
+    say("  every head's rows below 4096 against src_of")
+    for l in range(12):  # one layer (16 batches) at a time: the index tensor stays small
+        b0, b1 = 16 * l, 16 * (l + 1)
+        idx = src_of[b0:b1].long()[..., None].expand(-1, -1, -1, d.D)
+        for new, old in ((x["K"], K0), (x["V"], V0)):
+            assert torch.equal(new[b0:b1, :, : d.n_keep].view(torch.int16), old[b0:b1].gather(2, idx).view(torch.int16))
+    del K0, V0
+    hl = [(bsel.index(b), h) for b, h in heads]
+    say(f"  oracle on {len(hl)} heads")
+    ref = oracle.evict(xh["K"], xh["V"], xh["q_win"], xh["beacons"], xh["counts"], N=w.N, budget=w.budget, W=w.W,
+                       rope_cos=xh["rope_cos"], rope_sin=xh["rope_sin"], heads=hl, threads=len(hl))
+    for (b, h), (lb, _) in zip(heads, hl):
+        assert_scores_close(s_all[b, h], ref["scores"][lb, h])
+        kg = k_all[b, h]
+        band, diff = compare_kept(kg[None], ref["kept"][lb, h][None], ref["scores"][lb, h][None], w.N, w.W, 0,
+                                  w.budget)
+        say(f"  head ({b}, {h}): tie band {band}, {diff} in-band differences")
+        kf, vf, so, moved = oracle.compact_fill(xh["K"][lb:lb + 1, h:h + 1], xh["V"][lb:lb + 1, h:h + 1],
+                                                kg[None, None], w.N)
+        assert np.array_equal(raw_bits(x["K"][b, h]), kf[0, 0])
+        assert np.array_equal(raw_bits(x["V"][b, h]), vf[0, 0])
+        assert np.array_equal(so_all[b, h], so[0, 0])
+        say(f"  head ({b}, {h}): {int(moved[0, 0])} rows moved")
