@@ -182,24 +182,35 @@ __global__ __launch_bounds__(64 * NW) void beacon_update_kernel(const T* __restr
                     bn2[chosen] = xn;
                 }
             } else {
-                // argmax over the slots, ties -> lowest slot: the minimum of
-                // (inverted order key of the cosine, slot)
-                unsigned long long key = ~0ull;
+                // argmax over the slots, ties -> lowest slot: the smallest
+                // inverted order key of the cosine over the wave, then the
+                // lowest lane that holds it.  The cosine takes hardware
+                // reciprocal square roots (about 1 ulp each), so the choice can
+                // differ from exact arithmetic only where the two best cosines
+                // lie within a few 1e-7 of each other.
+                const float rx = __builtin_amdgcn_rsqf(xn);
+                auto cosine = [&](float dot, float bn) {
+                    return (xn == 0.f || bn == 0.f) ? 0.f : dot * rx * __builtin_amdgcn_rsqf(bn);
+                };
+                unsigned key = ~0u;
+                bool holds;  // this lane speaks for a slot
+                int shift;   // lane -> slot
                 if constexpr (NW == 1) {
                     // C <= 16: lanes 4c .. 4c+3 each take a quarter of slot c
                     const int c = lane >> 2, part = lane & 3;
                     const float dot = dev::quad_sum(c < C ? row_dot<QD>(&bl[c * LD + part * QD], &xs[part * QD]) : 0.f);
-                    const float bn = (c < C) ? bn2[c] : 0.f;
-                    const float cs = (xn == 0.f || bn == 0.f) ? 0.f : dot / (sqrtf(xn) * sqrtf(bn));
-                    if (c < C && part == 0) key = ((unsigned long long)(~dev::ord_key(cs)) << 32) | (unsigned)c;
+                    holds = c < C && part == 0;
+                    if (holds) key = ~dev::ord_key(cosine(dot, bn2[c]));
+                    shift = 2;
                 } else {
                     // lane c takes slot c
                     const float dot = (lane < C) ? row_dot<D>(&bl[lane * LD], xs) : 0.f;
-                    const float bn = (lane < C) ? bn2[lane] : 0.f;
-                    const float cs = (xn == 0.f || bn == 0.f) ? 0.f : dot / (sqrtf(xn) * sqrtf(bn));
-                    if (lane < C) key = ((unsigned long long)(~dev::ord_key(cs)) << 32) | (unsigned)lane;
+                    holds = lane < C;
+                    if (holds) key = ~dev::ord_key(cosine(dot, bn2[lane]));
+                    shift = 0;
                 }
-                chosen = (int)(unsigned)dev::wave_min_u64(key);
+                const unsigned kmin = dev::wave_min_u32(key);
+                chosen = (__ffsll(__ballot(holds && key == kmin)) - 1) >> shift;
                 const int n = cnt[chosen] + 1;
                 const float inv = 1.0f / (float)n;
                 float p = 0.f;
