@@ -88,6 +88,9 @@ def parse():
                     help="time only the 32K layer's stages one by one (score, top-k, compaction, fused eviction; "
                          "10 repetitions) and the scoring options, print them as one JSON line; for profiling "
                          "those kernels alone")
+    ap.add_argument("--only-decode-trace", action="store_true",
+                    help="run only the 36-layer decode trace (both compactions) and print it as one JSON line; "
+                         "for profiling its stacked kernels alone")
     ap.add_argument("--calibrate", action="store_true",
                     help="first run an untimed elementwise negate of 1 GiB bf16 (1 GiB read, 1 GiB written) "
                          "whose hardware counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -125,6 +128,9 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    if args.only_decode_trace:
+        print(json.dumps({"decode_trace": decode_trace_measure(w, dev)}), flush=True)
+        return
     if args.only_stages:
         res = {"stages": stages_measure(w, dev, reps=10)}
         lay = [synth.make_layer(w, seed=l, device=dev) for l in range(6)]

@@ -10,23 +10,24 @@
 // Sources lie at or above n and destinations below it, so no move can read
 // a row another move writes: the copy needs no ordering at all.  One
 // workgroup per head first writes src_of (the old position of the row each
-// position ends up with), then a grid of 64-row items copies the rows whose
-// src_of differs from their position.
+// position ends up with), then a grid of items of 1024 positions copies the
+// rows whose src_of differs from their position.
 //
 // src_of: a bitmap of the kept positions below n goes to LDS; position p
-// is a hole of rank m = p - (kept positions below p), counted with a block
-// scan of the bitmap words' popcounts, and takes kept[c + m], c being the
-// number of kept rows below n.
+// is a hole of rank m = p - (kept positions below p), counted from a block
+// scan of the bitmap words' popcounts and the popcount of p's word below p,
+// and takes kept[c + m], c being the number of kept rows below n.
 #include "device_common.h"
 #include "internal.h"
 
 namespace bkv {
 namespace {
 
-constexpr int kMapThreads = 1024;
+constexpr int kMapThreads = 256;  // small workgroups: many heads in flight per compute unit
 constexpr int kMapWaves = kMapThreads / 64;
 constexpr int kCopyThreads = 256;
-constexpr int kCopyRows = 64;
+constexpr int kCopyItem = 1024;  // positions per copy work item
+constexpr int kCopyRows = 64;    // rows copied per pass
 
 // Exclusive scan of one int per thread over the block; buf holds kMapWaves ints.
 __device__ __forceinline__ int block_excl_scan(int v, int* buf) {
@@ -49,6 +50,7 @@ __global__ __launch_bounds__(kMapThreads) void fill_map_kernel(const int32_t* __
                                                                int32_t* __restrict__ src_of, int N, int n_keep,
                                                                int P, int budget, int* hdr) {
     __shared__ uint32_t bits[kMaxFillKeep / 32];
+    __shared__ int wpre[kMaxFillKeep / 32];  // kept positions below each word
     __shared__ int scan_buf[kMapWaves];
     __shared__ int s_c, s_bad, s_ok;
     const int h = blockIdx.x, tid = threadIdx.x;
@@ -81,59 +83,84 @@ __global__ __launch_bounds__(kMapThreads) void fill_map_kernel(const int32_t* __
         return;
     }
     const int c = s_c;
-    // thread t walks the bitmap words [w0, w1), in order
+    // kept positions below each bitmap word: thread t takes the words
+    // [w0, w1), a block scan gives the count below w0
     const int wpt = (nw + kMapThreads - 1) / kMapThreads;
     const int w0 = min(tid * wpt, nw), w1 = min(w0 + wpt, nw);
     int mine = 0;
     for (int w = w0; w < w1; ++w) mine += __builtin_popcount(bits[w]);
-    int kept_below = block_excl_scan(mine, scan_buf);  // kept positions below word w0
+    int below_w = block_excl_scan(mine, scan_buf);
     for (int w = w0; w < w1; ++w) {
-        const uint32_t b = bits[w];
-        for (int i = 0; i < 32; ++i) {
-            const int p = w * 32 + i;
-            if (p >= n_keep) break;
-            if ((b >> i) & 1u) {
-                so[p] = p;
-                ++kept_below;
-            } else {
-                so[p] = kh[c + (p - kept_below)];  // hole of rank p - kept_below
-            }
+        wpre[w] = below_w;
+        below_w += __builtin_popcount(bits[w]);
+    }
+    __syncthreads();
+    // one position per thread and pass: coalesced stores, independent loads
+    for (int p = tid; p < n_keep; p += kMapThreads) {
+        const uint32_t b = bits[p >> 5];
+        const int i = p & 31;
+        if ((b >> i) & 1u) {
+            so[p] = p;
+        } else {
+            const int kept_below = wpre[p >> 5] + __builtin_popcount(b & ((1u << i) - 1u));
+            so[p] = kh[c + (p - kept_below)];  // hole of rank p - kept_below
         }
     }
 }
 
-// RB = row bytes; VPR = 16-byte vectors per row.  Item (head, chunk) moves
-// the rows of positions [64 chunk, 64 chunk + 64) whose source differs.
+// RB = row bytes; VPR = 16-byte vectors per row.  Item (head, chunk) lists
+// the moves among positions [kCopyItem chunk, + kCopyItem) (those whose
+// src_of differs from the position) in LDS, in any order, then copies them
+// kCopyRows rows per pass.  Items sized by positions rather than by moves
+// keep the grid small where few rows move (the steady state of a periodic
+// eviction moves a few per cent of them).
 template <int RB>
 __global__ __launch_bounds__(kCopyThreads) void fill_copy_kernel(char* K, char* V, const int32_t* __restrict__ src_of,
                                                                  int n_keep, int nchunk, size_t head_stride) {
     constexpr int VPR = RB / 16;
-    constexpr int NV = 2 * kCopyRows * VPR / kCopyThreads;  // 16-byte vectors per thread (K and V)
-    __shared__ int s_src[kCopyRows];
+    constexpr int NV = 2 * kCopyRows * VPR / kCopyThreads;  // 16-byte vectors per thread and pass (K and V)
+    static_assert(2 * kCopyRows * VPR % kCopyThreads == 0, "whole vectors per thread");
+    __shared__ int s_src[kCopyItem], s_dst[kCopyItem];
+    __shared__ int s_n;
     const int h = blockIdx.x / nchunk, ch = blockIdx.x - h * nchunk;
-    const int j0 = ch * kCopyRows, rows = min(kCopyRows, n_keep - j0);
+    const int j0 = ch * kCopyItem, rows = min(kCopyItem, n_keep - j0);
     const int tid = threadIdx.x;
-    if (tid < rows) s_src[tid] = src_of[(size_t)h * n_keep + j0 + tid];
+    if (tid == 0) s_n = 0;
     __syncthreads();
+    for (int r = tid; r < rows; r += kCopyThreads) {
+        const int src = src_of[(size_t)h * n_keep + j0 + r];
+        if (src != j0 + r) {
+            const int slot = atomicAdd(&s_n, 1);  // at most rows slots
+            s_src[slot] = src;
+            s_dst[slot] = j0 + r;
+        }
+    }
+    __syncthreads();
+    const int nm = s_n;
     char* Kh = K + (size_t)h * head_stride;
     char* Vh = V + (size_t)h * head_stride;
-    dev::u32x4 buf[NV];
-    dev::static_for<NV>([&](auto kc) {
-        constexpr int k = decltype(kc)::value;
-        const int e = tid + k * kCopyThreads;
-        const int which = e / (kCopyRows * VPR);
-        const int r = (e / VPR) % kCopyRows, v = e % VPR;
-        if (r < rows && s_src[r] != j0 + r)
-            buf[k] = __builtin_nontemporal_load(reinterpret_cast<const dev::u32x4*>((which ? Vh : Kh) + (size_t)s_src[r] * RB) + v);
-    });
-    dev::static_for<NV>([&](auto kc) {
-        constexpr int k = decltype(kc)::value;
-        const int e = tid + k * kCopyThreads;
-        const int which = e / (kCopyRows * VPR);
-        const int r = (e / VPR) % kCopyRows, v = e % VPR;
-        if (r < rows && s_src[r] != j0 + r)
-            __builtin_nontemporal_store(buf[k], reinterpret_cast<dev::u32x4*>((which ? Vh : Kh) + (size_t)(j0 + r) * RB) + v);
-    });
+    for (int m0 = 0; m0 < nm; m0 += kCopyRows) {
+        const int mr = min(kCopyRows, nm - m0);
+        dev::u32x4 buf[NV];
+        dev::static_for<NV>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            const int e = tid + k * kCopyThreads;
+            const int which = e / (kCopyRows * VPR);
+            const int r = (e / VPR) % kCopyRows, v = e % VPR;
+            if (r < mr)
+                buf[k] = __builtin_nontemporal_load(
+                    reinterpret_cast<const dev::u32x4*>((which ? Vh : Kh) + (size_t)s_src[m0 + r] * RB) + v);
+        });
+        dev::static_for<NV>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            const int e = tid + k * kCopyThreads;
+            const int which = e / (kCopyRows * VPR);
+            const int r = (e / VPR) % kCopyRows, v = e % VPR;
+            if (r < mr)
+                __builtin_nontemporal_store(
+                    buf[k], reinterpret_cast<dev::u32x4*>((which ? Vh : Kh) + (size_t)s_dst[m0 + r] * RB) + v);
+        });
+    }
 }
 
 }  // namespace
@@ -145,7 +172,7 @@ hipError_t launch_compact_fill(const bkv_dims& d, void* K, void* V, const int32_
     if (P == 0 || n_keep == 0) return hipSuccess;
     hipLaunchKernelGGL(fill_map_kernel, dim3(P), dim3(kMapThreads), 0, s, kept, src_of, d.N, n_keep, P, d.budget,
                        static_cast<int*>(ws));
-    const int nchunk = (n_keep + kCopyRows - 1) / kCopyRows;
+    const int nchunk = (n_keep + kCopyItem - 1) / kCopyItem;
     const int es = d.dtype == BKV_BF16 ? 2 : 4;
     const int rb = d.D * es;
     const size_t hs = (size_t)d.N_cap * rb;
