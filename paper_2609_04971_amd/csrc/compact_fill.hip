@@ -67,6 +67,7 @@ __global__ __launch_bounds__(kMapThreads) void fill_map_kernel(const int32_t* __
     }
     __syncthreads();
     int below = 0;  // kept positions below n seen by this thread
+#pragma unroll 4
     for (int i = tid; i < n_keep; i += kMapThreads) {
         const int k = kh[i];
         if (k < 0 || k >= N || (i > 0 && k <= kh[i - 1])) s_bad = 1;  // benign race: any writer stores 1
@@ -95,16 +96,16 @@ __global__ __launch_bounds__(kMapThreads) void fill_map_kernel(const int32_t* __
         below_w += __builtin_popcount(bits[w]);
     }
     __syncthreads();
-    // one position per thread and pass: coalesced stores, independent loads
+    // one position per thread and pass: coalesced stores, and loads that
+    // do not wait on one another (a kept position loads kept[0], unused)
+#pragma unroll 4
     for (int p = tid; p < n_keep; p += kMapThreads) {
         const uint32_t b = bits[p >> 5];
         const int i = p & 31;
-        if ((b >> i) & 1u) {
-            so[p] = p;
-        } else {
-            const int kept_below = wpre[p >> 5] + __builtin_popcount(b & ((1u << i) - 1u));
-            so[p] = kh[c + (p - kept_below)];  // hole of rank p - kept_below
-        }
+        const bool stays = (b >> i) & 1u;
+        const int kept_below = wpre[p >> 5] + __builtin_popcount(b & ((1u << i) - 1u));
+        const int from = kh[stays ? 0 : c + (p - kept_below)];  // hole of rank p - kept_below
+        so[p] = stays ? p : from;
     }
 }
 
